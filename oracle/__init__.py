@@ -1,0 +1,204 @@
+"""ctypes loader for the CPU oracle (``oracle.cpp``).
+
+TEST INFRASTRUCTURE ONLY: the test suite, the smoke check and the benchmark's
+CPU-baseline leg are the only users.  The product path never imports this
+package.  Functions take the seeded generator's plain arrays; see
+``oracle.cpp`` for what each one computes and which passage of the paper it
+follows.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from dataclasses import dataclass
+from typing import Optional, Tuple
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+SRC = os.path.join(HERE, "oracle.cpp")
+LIB = os.path.join(HERE, "liboracle.so")
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with the host compiler (plain g++, -O2)."""
+    if force or not os.path.exists(LIB) or os.path.getmtime(LIB) < os.path.getmtime(SRC):
+        tmp = LIB + ".tmp"
+        subprocess.check_call(["g++", "-O2", "-std=c++17", "-fPIC", "-shared", "-o", tmp, SRC, "-lpthread"])
+        os.replace(tmp, LIB)
+    return LIB
+
+
+class _Lexer(ctypes.Structure):
+    _fields_ = [("num_states", ctypes.c_int32), ("trans", ctypes.c_void_p), ("accept", ctypes.c_void_p)]
+
+
+class _Grammar(ctypes.Structure):
+    _fields_ = [("num_terminals", ctypes.c_int32), ("num_nonterminals", ctypes.c_int32),
+                ("start", ctypes.c_int32), ("num_productions", ctypes.c_int32),
+                ("lhs", ctypes.c_void_p), ("rhs_offsets", ctypes.c_void_p), ("rhs", ctypes.c_void_p)]
+
+
+class _Vocab(ctypes.Structure):
+    _fields_ = [("vocab_size", ctypes.c_int32), ("bytes", ctypes.c_void_p), ("offsets", ctypes.c_void_p)]
+
+
+_lib: Optional[ctypes.CDLL] = None
+
+
+def lib() -> ctypes.CDLL:
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB) or os.path.getmtime(LIB) < os.path.getmtime(SRC):
+            build(force=True)
+        L = ctypes.CDLL(LIB)
+        P = ctypes.c_void_p
+        i32 = ctypes.c_int
+        L.oracle_lex_step.argtypes = [P, i32, i32, P]
+        L.oracle_lex_bytes.argtypes = [P, i32, P, i32, i32, P, i32, P]
+        L.oracle_memo.argtypes = [P, P, P]
+        L.oracle_valid.argtypes = [P, P, P, P, i32]
+        L.oracle_cover.argtypes = [P, P, P, P, i32]
+        L.oracle_dfa_states.argtypes = [P, P, P, P, i32]
+        L.oracle_validate_batch.argtypes = [P, P, P, P, i32, i32, P, P, P, i32, P, i32]
+        L.oracle_select.argtypes = [P, P, P, P, i32, i32, P, P, P, P, P, i32, P, P, i32]
+        _lib = L
+    return _lib
+
+
+def _ptr(a: np.ndarray) -> int:
+    return a.ctypes.data
+
+
+@dataclass
+class Problem:
+    """Lexer DFA, grammar and vocabulary as contiguous arrays plus C structs."""
+
+    trans: np.ndarray
+    accept: np.ndarray
+    T: int
+    N: int
+    start: int
+    lhs: np.ndarray
+    roff: np.ndarray
+    rhs: np.ndarray
+    vbytes: np.ndarray
+    voffs: np.ndarray
+
+    def __post_init__(self):
+        self.trans = np.ascontiguousarray(self.trans, dtype=np.int16)
+        self.accept = np.ascontiguousarray(self.accept, dtype=np.int16)
+        self.lhs = np.ascontiguousarray(self.lhs, dtype=np.int32)
+        self.roff = np.ascontiguousarray(self.roff, dtype=np.int32)
+        self.rhs = np.ascontiguousarray(self.rhs, dtype=np.int32)
+        self.vbytes = np.ascontiguousarray(self.vbytes, dtype=np.uint8)
+        if self.vbytes.size == 0:
+            self.vbytes = np.zeros(1, dtype=np.uint8)
+        self.voffs = np.ascontiguousarray(self.voffs, dtype=np.int32)
+        self._lx = _Lexer(self.trans.shape[0], _ptr(self.trans), _ptr(self.accept))
+        self._gr = _Grammar(self.T, self.N, self.start, len(self.lhs), _ptr(self.lhs), _ptr(self.roff),
+                            _ptr(self.rhs) if self.rhs.size else _ptr(np.zeros(1, np.int32)))
+        self._vc = _Vocab(len(self.voffs) - 1, _ptr(self.vbytes), _ptr(self.voffs))
+
+    @property
+    def Q(self) -> int:
+        return int(self.trans.shape[0])
+
+    @property
+    def V(self) -> int:
+        return len(self.voffs) - 1
+
+    @property
+    def refs(self):
+        return ctypes.byref(self._lx), ctypes.byref(self._gr), ctypes.byref(self._vc)
+
+
+def problem_from(lang, vocab) -> Problem:
+    """Build a Problem from a grammars.Language and a workloads.Vocab."""
+    tb = lang.tables
+    T, N, start, lhs, roff, rhs = lang.grammar.arrays()
+    vb, vo = vocab.csr()
+    return Problem(tb.trans, tb.accept, T, N, start, lhs, roff, rhs, vb, vo)
+
+
+def lex_step(p: Problem, q: int, c: int) -> Tuple[int, int]:
+    e = ctypes.c_int(0)
+    r = lib().oracle_lex_step(ctypes.byref(p._lx), q, c, ctypes.byref(e))
+    return r, e.value
+
+
+def lex_bytes(p: Problem, q: int, data: bytes, flush: bool):
+    """(terminals, final_state) or None if the greedy lexer dies."""
+    buf = np.frombuffer(data, dtype=np.uint8).copy() if data else np.zeros(1, np.uint8)
+    out = np.zeros(len(data) + 2, dtype=np.int32)
+    fs = ctypes.c_int(-1)
+    n = lib().oracle_lex_bytes(ctypes.byref(p._lx), q, _ptr(buf), len(data), int(flush), _ptr(out), len(out),
+                               ctypes.byref(fs))
+    if n < 0:
+        return None
+    return out[:n].tolist(), fs.value
+
+
+def memo(p: Problem) -> np.ndarray:
+    out = np.zeros((p.V, p.Q, 16), dtype=np.uint8)
+    r = lib().oracle_memo(ctypes.byref(p._lx), ctypes.byref(p._vc), _ptr(out))
+    if r != 0:
+        raise ValueError("token longer than 8 bytes or empty")
+    return out
+
+
+def _seq(x) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(x, dtype=np.int32))
+
+
+def valid(p: Problem, x) -> int:
+    xs = _seq(x)
+    lx, gr, vc = p.refs
+    return lib().oracle_valid(lx, gr, vc, _ptr(xs) if xs.size else _ptr(np.zeros(1, np.int32)), int(xs.size))
+
+
+def cover(p: Problem, x) -> int:
+    xs = _seq(x)
+    lx, gr, vc = p.refs
+    return lib().oracle_cover(lx, gr, vc, _ptr(xs) if xs.size else _ptr(np.zeros(1, np.int32)), int(xs.size))
+
+
+def dfa_states(p: Problem, x) -> int:
+    xs = _seq(x)
+    lx, gr, vc = p.refs
+    return lib().oracle_dfa_states(lx, gr, vc, _ptr(xs) if xs.size else _ptr(np.zeros(1, np.int32)), int(xs.size))
+
+
+def _cands(seq, pos, tok):
+    return _seq(seq), _seq(pos), _seq(tok)
+
+
+def validate_batch(p: Problem, seqs: np.ndarray, seq, pos, tok, nthreads: int = 1) -> np.ndarray:
+    s = np.ascontiguousarray(seqs, dtype=np.int32)
+    cs, cp, ct = _cands(seq, pos, tok)
+    C = int(cs.size)
+    out = np.zeros(max(C, 1), dtype=np.uint8)
+    lx, gr, vc = p.refs
+    r = lib().oracle_validate_batch(lx, gr, vc, _ptr(s), s.shape[0], s.shape[1], _ptr(cs) if C else 0,
+                                    _ptr(cp) if C else 0, _ptr(ct) if C else 0, C, _ptr(out), nthreads)
+    if r != 0:
+        raise RuntimeError(f"oracle_validate_batch failed ({r})")
+    return out[:C]
+
+
+def select(p: Problem, seqs: np.ndarray, seq, pos, tok, conf, verdict, nthreads: int = 1):
+    """Returns (selected uint8[C], (cover_calls, exact_calls), status)."""
+    s = np.ascontiguousarray(seqs, dtype=np.int32)
+    cs, cp, ct = _cands(seq, pos, tok)
+    cf = np.ascontiguousarray(conf, dtype=np.float32)
+    vd = np.ascontiguousarray(verdict, dtype=np.uint8)
+    C = int(cs.size)
+    out = np.zeros(max(C, 1), dtype=np.uint8)
+    stats = np.zeros(2, dtype=np.int64)
+    lx, gr, vc = p.refs
+    if C == 0:
+        return out[:0], (0, 0), 0
+    r = lib().oracle_select(lx, gr, vc, _ptr(s), s.shape[0], s.shape[1], _ptr(cs), _ptr(cp), _ptr(ct), _ptr(cf),
+                            _ptr(vd), C, _ptr(out), _ptr(stats), nthreads)
+    return out[:C], (int(stats[0]), int(stats[1])), int(r)
