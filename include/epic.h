@@ -1,0 +1,167 @@
+/* epic.h - C ABI of the MI355X (gfx950) validity-check hot path of EPIC
+ * (Efficient and Parallel Inference under CFG constraints, arxiv 2606.00722).
+ *
+ * Per denoising step a diffusion LM proposes (position, token) commits for a
+ * batch of partially masked token sequences.  This library decides, for every
+ * proposal, whether the sequence stays completable under a context-free
+ * grammar (Sec. 3: Valid_G(x, D) = 1[L(G) cap C_{x+D} != empty], masked runs
+ * read as Sigma*), and then chooses the relaxed compatible subset of the
+ * valid proposals to commit together (Sec. 4.3, Alg. 4).
+ *
+ * Conventions for every call:
+ *  - Pointers named d_* are device pointers (HIP device memory, e.g. PyTorch
+ *    tensors); all other pointers are host pointers.  Host data is copied
+ *    before the call returns; the caller keeps ownership of everything it
+ *    passes in.
+ *  - Device work is enqueued on `stream` and the call returns without
+ *    waiting; outputs are valid after the stream is synchronised.
+ *  - A context is used by one host thread at a time; distinct contexts are
+ *    independent.  Calls on one context that overlap on different streams
+ *    must not share a workspace.
+ *  - Errors detectable on the host are returned immediately as a negative
+ *    epic_status and nothing is enqueued.  Errors that only the device can
+ *    see mark the affected candidate (verdict 2) and set a sticky device flag
+ *    that epic_ctx_device_error() reads after synchronising.
+ */
+#ifndef EPIC_H
+#define EPIC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  EPIC_OK = 0,
+  EPIC_ERR_NULL = -1,        /* a required pointer is NULL */
+  EPIC_ERR_ARG = -2,         /* a size or index argument is out of range */
+  EPIC_ERR_CAPACITY = -3,    /* larger than the context or workspace was sized for */
+  EPIC_ERR_LEXER = -4,       /* lexer DFA malformed (start accepts, not trim, bad label) */
+  EPIC_ERR_GRAMMAR = -5,     /* undefined symbol, start not a nonterminal, too large */
+  EPIC_ERR_VOCAB = -6,       /* token empty or longer than 8 bytes */
+  EPIC_ERR_HIP = -7,         /* a HIP runtime call failed */
+  EPIC_ERR_STATE = -8,       /* memo not built yet */
+  EPIC_ERR_UNSUPPORTED = -9  /* outside the sizes this build supports (see below) */
+} epic_status;
+
+/* Device-side sticky error bits, read by epic_ctx_device_error(). */
+#define EPIC_DEV_BAD_CANDIDATE 1u  /* position not masked, token/sequence/position out of range */
+#define EPIC_DEV_CAPACITY 2u       /* a chart or graph buffer overflowed: verdict 2 written */
+#define EPIC_DEV_BAD_SELECT 4u     /* duplicate positions or NaN confidence among valid candidates */
+
+typedef struct epic_ctx epic_ctx;
+
+/* Lexer DFA: the compiled lexical map (Alg. 1 "compile the lexical map").
+ * States 0..num_states-1, state 0 is the start state and must not accept;
+ * every state must reach an accepting state (trim).  trans[q*256 + byte] is
+ * the successor or -1.  accept[q] is -1 (not accepting), -2 (a skip lexeme
+ * such as whitespace) or a grammar terminal id.  Lexing is greedy with one
+ * byte of lookahead and no backtracking: a lexeme ends when the next byte has
+ * no transition; the earlier-listed rule already decided the label.
+ * Supported: num_states <= 256. */
+typedef struct {
+  int32_t num_states;
+  const int16_t* trans;
+  const int16_t* accept;
+} epic_lexer_desc;
+
+/* Grammar G = (V, Sigma_lex, P, S) (Sec. 3).  Terminals are 0..T-1,
+ * nonterminals T..T+N-1; production p is lhs[p] -> rhs[rhs_offsets[p] ..
+ * rhs_offsets[p+1]).  Empty right-hand sides are allowed.
+ * Supported: T <= 63, N <= 64, at most 1024 dotted items (sum of |rhs|+1). */
+typedef struct {
+  int32_t num_terminals, num_nonterminals, start, num_productions;
+  const int32_t* lhs;
+  const int32_t* rhs_offsets;
+  const int32_t* rhs;
+} epic_grammar_desc;
+
+/* Tokenizer vocabulary Gamma: token t has bytes[offsets[t] .. offsets[t+1]),
+ * 1 to 8 bytes. */
+typedef struct {
+  int32_t vocab_size;
+  const uint8_t* bytes;
+  const int32_t* offsets;
+} epic_vocab_desc;
+
+/* Create a context: validates the descriptors, builds the constant tables
+ * (dotted items, prediction closure, the lexer's gap automaton reduced to its
+ * left-language classes, the regular cover of App. A.2), uploads them and
+ * allocates the memo table (vocab_size * num_states * 16 bytes).  max_batch,
+ * max_seq_len and max_cands bound later calls.  *out receives the context. */
+epic_status epic_ctx_create(const epic_lexer_desc* lexer, const epic_grammar_desc* grammar,
+                            const epic_vocab_desc* vocab, int32_t max_batch, int32_t max_seq_len,
+                            int32_t max_cands, epic_ctx** out);
+
+void epic_ctx_destroy(epic_ctx* ctx);
+
+/* Bytes of device workspace that epic_validate_batch and
+ * epic_select_compatible need (the caller allocates it, 256-byte aligned). */
+size_t epic_workspace_bytes(const epic_ctx* ctx);
+
+/* Number of gap classes of the lexer (diagnostics; 1 for lexers whose
+ * whitespace can separate any two lexemes). */
+int32_t epic_gap_classes(const epic_ctx* ctx);
+
+/* Alg. 2, lexing memoization: for every token t and lexer state q the greedy
+ * lexing of t's bytes from q, without a final flush, into the context's memo
+ * table.  Entry (t, q) sits at byte offset (t*num_states + q)*16:
+ *   [0..1] state after the token (little-endian u16, 0xFFFF = the lexer dies)
+ *   [2]    number of emissions (skip lexemes included)
+ *   [3]    emission mask: bit j set when reading byte j ended a lexeme
+ *   [4..11] emitted labels in order (terminal id, 0xFF = skip), unused = 0
+ *   [12..15] zero.  A dead entry is all zero except bytes 0..1.
+ * Enqueued on `stream`; must complete before validation reads the memo. */
+epic_status epic_lexmemo_build(epic_ctx* ctx, hipStream_t stream);
+
+/* Copy the memo table to host memory (bytes >= vocab_size*num_states*16).
+ * Synchronous. */
+epic_status epic_memo_export(const epic_ctx* ctx, void* host_dst, size_t bytes);
+
+/* Validity of each proposal (Sec. 3 Valid; Alg. 3 is the recogniser):
+ * verdict[c] = Valid_G(x_b, {(pos[c], tok[c])}) for b = cand_seq[c], i.e. 1
+ * if x_b with token tok[c] at position pos[c] can still be completed into a
+ * sentence of L(G), else 0; 2 if the candidate is malformed (sequence or
+ * position out of range, position not masked in x_b, token out of range).
+ * d_seqs: int32 [B*n] row-major, -1 = MASK.  d_cand_*: int32 [C].
+ * d_verdict: uint8 [C].  Every candidate is judged against the same x_b.
+ * d_workspace: at least epic_workspace_bytes(ctx) bytes. */
+epic_status epic_validate_batch(epic_ctx* ctx, const int32_t* d_seqs, int32_t B, int32_t n,
+                                const int32_t* d_cand_seq, const int32_t* d_cand_pos,
+                                const int32_t* d_cand_tok, int32_t C, uint8_t* d_verdict,
+                                void* d_workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Relaxed compatible-subset selection (Alg. 4): per sequence, the candidates
+ * with verdict 1 are sorted by descending confidence (float32, ties to the
+ * lower candidate index) and passed to RelaxedSelect followed by
+ * ExactShrink; halves put the first ceil(|C|/2) candidates on the
+ * high-confidence side.  The relaxed check is the emptiness test of the
+ * regular cover intersected with the completion automaton (App. A.2);
+ * the exact check is Valid.  d_selected: uint8 [C], 1 = in the returned
+ * subset B (empty, or at least two candidates whose joint application is
+ * exactly valid).  A sequence whose verdict-1 candidates repeat a position or
+ * carry a NaN confidence selects nothing and sets EPIC_DEV_BAD_SELECT.
+ * d_counts (optional, device int64 [2]) accumulates the number of cover and
+ * exact checks performed. */
+epic_status epic_select_compatible(epic_ctx* ctx, const int32_t* d_seqs, int32_t B, int32_t n,
+                                   const int32_t* d_cand_seq, const int32_t* d_cand_pos,
+                                   const int32_t* d_cand_tok, const float* d_conf,
+                                   const uint8_t* d_verdict, int32_t C, uint8_t* d_selected,
+                                   int64_t* d_counts, void* d_workspace, size_t workspace_bytes,
+                                   hipStream_t stream);
+
+/* Synchronise `stream`, then read and clear the sticky device error bits
+ * (EPIC_DEV_*) into *flags. */
+epic_status epic_ctx_device_error(epic_ctx* ctx, hipStream_t stream, uint32_t* flags);
+
+const char* epic_status_string(epic_status s);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* EPIC_H */

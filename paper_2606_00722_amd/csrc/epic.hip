@@ -1,0 +1,660 @@
+// libepic: MI355X (gfx950) implementation of the C ABI in include/epic.h.
+//
+// Kernels:
+//  * lexmemo_kernel  - Alg. 2's lexing memo as a dense table: one thread per
+//                      (token, lexer state), token-major so that the rows a
+//                      masked gap's exit reads (all states of one token) are
+//                      contiguous 16-byte entries.
+//  * validate_kernel - one workgroup per candidate (grid-stride over
+//                      candidates): the sequence with the candidate applied is
+//                      walked into its lexeme graph and recognised by the
+//                      Earley engine of walker.inc (Alg. 3).
+//  * select_kernel   - one workgroup per sequence runs Alg. 4 with an explicit
+//                      stack; every relaxed / exact check is a walk of the
+//                      same workgroup (cover policy / Earley policy).
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "../../include/epic.h"
+#include "tables.h"
+
+namespace epic {
+
+#define EPIC_DEV __device__ inline
+
+__device__ inline int tid() { return (int)threadIdx.x; }
+__device__ inline int nthreads() { return (int)blockDim.x; }
+__device__ inline void sync() { __syncthreads(); }
+__device__ inline uint32_t at_or32(uint32_t* p, uint32_t v) { return atomicOr(p, v); }
+__device__ inline uint64_t at_or64(uint64_t* p, uint64_t v) {
+  return (uint64_t)atomicOr((unsigned long long*)p, (unsigned long long)v);
+}
+__device__ inline int at_add32(int32_t* p, int v) { return atomicAdd(p, v); }
+__device__ inline uint32_t at_cas32(uint32_t* p, uint32_t cmp, uint32_t val) { return atomicCAS(p, cmp, val); }
+__device__ inline int at_min32(int32_t* p, int v) { return atomicMin(p, v); }
+
+#include "walker.inc"
+
+constexpr int kThreads = 256;
+
+// ------------------------------------------------------------------ memo
+__global__ void __launch_bounds__(kThreads) lexmemo_kernel(DevTab tb, uint4* memo) {
+  const size_t i = (size_t)blockIdx.x * kThreads + threadIdx.x;
+  if (i >= (size_t)tb.V * tb.Q) return;
+  const int t = (int)(i / tb.Q), q0 = (int)(i % tb.Q);
+  const int beg = tb.voffs[t], len = tb.voffs[t + 1] - beg;
+  int q = q0;
+  uint32_t n = 0, mask = 0, lab_lo = 0, lab_hi = 0;
+  bool dead = false;
+  for (int j = 0; j < len; ++j) {
+    const int c = tb.vbytes[beg + j];
+    const int d = tb.trans[q * 256 + c];
+    if (d >= 0) {
+      q = d;
+      continue;
+    }
+    const int a = tb.accept[q];
+    const int f = tb.trans[c];
+    if (a == -1 || f < 0) {
+      dead = true;
+      break;
+    }
+    const uint32_t lab = a == -2 ? 0xFFu : (uint32_t)a;
+    if (n < 4)
+      lab_lo |= lab << (8 * n);
+    else
+      lab_hi |= lab << (8 * (n - 4));
+    mask |= 1u << j;
+    ++n;
+    q = f;
+  }
+  uint4 e;
+  if (dead) {
+    e = make_uint4(0xFFFFu, 0u, 0u, 0u);
+  } else {
+    e = make_uint4((uint32_t)q | (n << 16) | (mask << 24), lab_lo, lab_hi, 0u);
+  }
+  memo[i] = e;
+}
+
+struct WsArgs {
+  char* base;
+  size_t slot_bytes;
+  size_t off_cnt, off_org, off_sum, off_bits, off_cov, off_tqn, off_tqm;
+  int maxn, maxe, tcap;
+};
+
+__device__ inline WgWork slot_work(const WsArgs& a, int slot) {
+  char* b = a.base + (size_t)slot * a.slot_bytes;
+  WgWork w;
+  w.row_off = (int32_t*)b;
+  w.row_cnt = (int32_t*)(b + a.off_cnt);
+  w.ent_org = (uint16_t*)(b + a.off_org);
+  w.ent_sum = (uint64_t*)(b + a.off_sum);
+  w.ent_bits = (uint32_t*)(b + a.off_bits);
+  w.cov = (uint32_t*)(b + a.off_cov);
+  w.tq_node = (uint32_t*)(b + a.off_tqn);
+  w.tq_mask = (uint64_t*)(b + a.off_tqm);
+  w.maxn = a.maxn;
+  w.maxe = a.maxe;
+  w.tcap = a.tcap;
+  return w;
+}
+
+// ------------------------------------------------------------------ validate
+template <int W>
+__global__ void __launch_bounds__(kThreads) validate_kernel(DevTab tb, const int32_t* __restrict__ seqs, int B,
+                                                            int n, const int32_t* __restrict__ cseq,
+                                                            const int32_t* __restrict__ cpos,
+                                                            const int32_t* __restrict__ ctok, int C,
+                                                            uint8_t* __restrict__ verdict, WsArgs ws) {
+  __shared__ Lds<W> L;
+  const WgWork wk = slot_work(ws, blockIdx.x);
+  for (int c = blockIdx.x; c < C; c += gridDim.x) {
+    const int b = cseq[c], i = cpos[c], t = ctok[c];
+    const bool bad = b < 0 || b >= B || i < 0 || i >= n || t < 0 || t >= tb.V || seqs[(size_t)b * n + i] >= 0;
+    if (bad) {
+      if (threadIdx.x == 0) {
+        verdict[c] = 2;
+        atomicOr(tb.dev_err, (uint32_t)EPIC_DEV_BAD_CANDIDATE);
+      }
+      continue;
+    }
+    if (threadIdx.x == 0) L.sel_bad = 0;
+    __syncthreads();
+    for (int k = threadIdx.x; k < n; k += kThreads) {
+      const int x = k == i ? t : seqs[(size_t)b * n + k];
+      if (x < -1 || x >= tb.V) L.sel_bad = 1;
+      L.xtok[k] = x;
+    }
+    __syncthreads();
+    if (L.sel_bad) {  // a token of the sequence is out of range
+      if (threadIdx.x == 0) {
+        verdict[c] = 2;
+        atomicOr(tb.dev_err, (uint32_t)EPIC_DEV_BAD_CANDIDATE);
+      }
+      __syncthreads();
+      continue;
+    }
+    const int r = walk<W, false>(tb, L, wk, n);
+    if (threadIdx.x == 0) {
+      verdict[c] = (uint8_t)(r < 0 ? 2 : r);
+      if (r < 0) atomicOr(tb.dev_err, (uint32_t)EPIC_DEV_CAPACITY);
+    }
+    __syncthreads();
+  }
+}
+
+// ------------------------------------------------------------------ select
+// Alg. 4 as a stack machine run by thread 0; checks are walks by the whole
+// workgroup.  Subsets are bit masks over the confidence-sorted candidates.
+enum : int { kRS = 0, kES = 1, kTop = 2 };
+enum : int { kReqNone = 0, kReqCover = 1, kReqExact = 2, kReqDone = 3 };
+
+struct Frame {
+  int type, stage;
+  uint64_t A, S, t1;
+};
+
+__device__ inline void split_halves(uint64_t S, uint64_t& lo, uint64_t& hi) {
+  int cnt = __popcll(S), h = (cnt + 1) / 2;  // ceil(|S|/2) on the high-confidence side
+  lo = 0;
+  uint64_t s = S;
+  for (int i = 0; i < h; ++i) {
+    uint64_t bit = s & (~s + 1);
+    lo |= bit;
+    s &= s - 1;
+  }
+  hi = S & ~lo;
+}
+
+template <int W>
+__global__ void __launch_bounds__(kThreads) select_kernel(DevTab tb, const int32_t* __restrict__ seqs, int B, int n,
+                                                          const int32_t* __restrict__ cseq,
+                                                          const int32_t* __restrict__ cpos,
+                                                          const int32_t* __restrict__ ctok,
+                                                          const float* __restrict__ conf,
+                                                          const uint8_t* __restrict__ verdict, int C,
+                                                          uint8_t* __restrict__ selected, long long* counts,
+                                                          WsArgs ws) {
+  __shared__ Lds<W> L;
+  __shared__ Frame stack[96];
+  __shared__ int sp;
+  __shared__ uint64_t ret_val, final_B;
+  const int b = blockIdx.x;
+  if (b >= B) return;
+  const WgWork wk = slot_work(ws, blockIdx.x);
+  if (threadIdx.x == 0) {
+    L.sel_n = 0;
+    L.sel_bad = 0;
+  }
+  __syncthreads();
+  for (int c = threadIdx.x; c < C; c += kThreads) {
+    if (cseq[c] != b) continue;
+    selected[c] = 0;
+    if (verdict[c] != 1) continue;
+    const int i = cpos[c], t = ctok[c];
+    if (i < 0 || i >= n || t < 0 || t >= tb.V || seqs[(size_t)b * n + i] >= 0) {
+      L.sel_bad = 3;  // a verdict-1 candidate that is not a legal update
+      continue;
+    }
+    int j = atomicAdd(&L.sel_n, 1);
+    if (j < 64) L.sel_idx[j] = c;
+  }
+  for (int k = threadIdx.x; k < n; k += kThreads) {
+    const int x = seqs[(size_t)b * n + k];
+    if (x < -1 || x >= tb.V) L.sel_bad = 3;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int m = L.sel_n;
+    if (L.sel_bad) {
+    } else if (m > 64) {
+      L.sel_bad = 2;
+    } else {
+      // order by candidate index, then stable sort by descending confidence
+      for (int i = 1; i < m; ++i)
+        for (int j = i; j > 0 && L.sel_idx[j - 1] > L.sel_idx[j]; --j) {
+          int tmp = L.sel_idx[j];
+          L.sel_idx[j] = L.sel_idx[j - 1];
+          L.sel_idx[j - 1] = tmp;
+        }
+      for (int i = 0; i < m; ++i) {
+        int c = L.sel_idx[i];
+        L.sel_pos[i] = cpos[c];
+        L.sel_tok[i] = ctok[c];
+        L.sel_conf[i] = conf[c];
+        if (!(L.sel_conf[i] == L.sel_conf[i])) L.sel_bad = 1;
+        for (int j = 0; j < i; ++j)
+          if (L.sel_pos[j] == L.sel_pos[i]) L.sel_bad = 1;
+      }
+      for (int i = 1; i < m; ++i)
+        for (int j = i; j > 0 && L.sel_conf[j - 1] < L.sel_conf[j]; --j) {
+          int ti = L.sel_idx[j];
+          L.sel_idx[j] = L.sel_idx[j - 1];
+          L.sel_idx[j - 1] = ti;
+          ti = L.sel_pos[j];
+          L.sel_pos[j] = L.sel_pos[j - 1];
+          L.sel_pos[j - 1] = ti;
+          ti = L.sel_tok[j];
+          L.sel_tok[j] = L.sel_tok[j - 1];
+          L.sel_tok[j - 1] = ti;
+          float tf = L.sel_conf[j];
+          L.sel_conf[j] = L.sel_conf[j - 1];
+          L.sel_conf[j - 1] = tf;
+        }
+    }
+    if (L.sel_bad)
+      atomicOr(tb.dev_err, L.sel_bad == 2   ? (uint32_t)EPIC_DEV_CAPACITY
+                           : L.sel_bad == 3 ? (uint32_t)EPIC_DEV_BAD_CANDIDATE
+                                            : (uint32_t)EPIC_DEV_BAD_SELECT);
+    sp = 0;
+    stack[0] = Frame{kTop, 0, 0, m >= 64 ? ~0ull : ((1ull << m) - 1), 0};
+    sp = 1;
+    ret_val = 0;
+    final_B = 0;
+  }
+  __syncthreads();
+  if (L.sel_bad) return;
+  long long ncover = 0, nexact = 0;
+  bool failed = false;
+  for (int step = 0; step < 1 << 20; ++step) {
+    if (threadIdx.x == 0) {
+      // run the machine until it needs a check or finishes
+      L.sel_req = kReqNone;
+      bool have_ret = false;
+      while (L.sel_req == kReqNone) {
+        if (sp == 0) {
+          L.sel_req = kReqDone;
+          break;
+        }
+        Frame& f = stack[sp - 1];
+        if (f.type == kTop) {
+          if (f.stage == 0) {
+            f.stage = 1;
+            stack[sp++] = Frame{kRS, 0, 0, f.S, 0};
+          } else if (f.stage == 1) {
+            f.stage = 2;
+            stack[sp++] = Frame{kES, 0, 0, ret_val, 0};
+          } else {
+            final_B = ret_val;
+            --sp;
+          }
+          continue;
+        }
+        const bool is_rs = f.type == kRS;
+        if (f.stage == 0) {
+          if (__popcll(f.S) <= 1) {
+            ret_val = 0;
+            --sp;
+            continue;
+          }
+          f.stage = 1;
+          L.sel_req = is_rs ? kReqCover : kReqExact;
+          L.sel_mask = f.A | f.S;
+          break;
+        }
+        if (f.stage == 1) {
+          if (L.sel_res) {
+            ret_val = f.S;
+            --sp;
+            continue;
+          }
+          uint64_t lo, hi;
+          split_halves(f.S, lo, hi);
+          f.stage = 2;
+          stack[sp++] = Frame{is_rs ? kRS : kES, 0, f.A, lo, 0};
+          continue;
+        }
+        if (f.stage == 2) {
+          uint64_t lo, hi;
+          split_halves(f.S, lo, hi);
+          f.t1 = ret_val;  // B_L (RelaxedSelect) or B'_L (ExactShrink)
+          f.stage = 3;
+          stack[sp++] = Frame{kRS, 0, f.A | f.t1, hi, 0};
+          continue;
+        }
+        if (f.stage == 3) {
+          if (is_rs) {
+            ret_val = f.t1 | ret_val;
+            --sp;
+            continue;
+          }
+          f.stage = 4;  // B'_R = ret_val; now ExactShrink(x + B'_L, B'_R)
+          stack[sp++] = Frame{kES, 0, f.A | f.t1, ret_val, 0};
+          continue;
+        }
+        // ExactShrink stage 4: B''_R = ret_val
+        ret_val = f.t1 | ret_val;
+        --sp;
+      }
+      (void)have_ret;
+      if (sp >= 95) L.sel_req = kReqDone;  // cannot happen for <= 64 candidates
+    }
+    __syncthreads();
+    const int req = L.sel_req;
+    if (req == kReqDone) break;
+    const uint64_t msk = L.sel_mask;
+    for (int k = threadIdx.x; k < n; k += kThreads) L.xtok[k] = seqs[(size_t)b * n + k];
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      for (int i = 0; i < L.sel_n; ++i)
+        if ((msk >> i) & 1) L.xtok[L.sel_pos[i]] = L.sel_tok[i];
+    }
+    __syncthreads();
+    int r;
+    if (req == kReqCover) {
+      r = walk<W, true>(tb, L, wk, n);
+      ++ncover;
+    } else {
+      r = walk<W, false>(tb, L, wk, n);
+      ++nexact;
+    }
+    if (r < 0) {
+      failed = true;
+      break;
+    }
+    if (threadIdx.x == 0) L.sel_res = r;
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    if (counts) {
+      atomicAdd((unsigned long long*)&counts[0], (unsigned long long)ncover);
+      atomicAdd((unsigned long long*)&counts[1], (unsigned long long)nexact);
+    }
+    if (failed) {
+      atomicOr(tb.dev_err, (uint32_t)EPIC_DEV_CAPACITY);
+    } else {
+      for (int i = 0; i < L.sel_n; ++i)
+        if ((final_B >> i) & 1) selected[L.sel_idx[i]] = 1;
+    }
+  }
+}
+
+}  // namespace epic
+
+// ==================================================================== C ABI
+using namespace epic;
+
+struct epic_ctx {
+  HostTables H;
+  int max_batch = 0, max_seq = 0, max_cands = 0;
+  int maxn = 0, maxe = 0, nslot = 0;
+  size_t slot_bytes = 0, ws_bytes = 0;
+  size_t off_cnt = 0, off_org = 0, off_sum = 0, off_bits = 0, off_cov = 0, off_tqn = 0, off_tqm = 0;
+  int tcap = 0;
+  void* d_tables = nullptr;
+  uint4* d_memo = nullptr;
+  uint32_t* d_err = nullptr;
+  DevTab tab{};
+  bool memo_built = false;
+  int device = 0;
+};
+
+namespace {
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+template <class T>
+size_t place(std::vector<char>& blob, const std::vector<T>& v) {
+  size_t off = align256(blob.size());
+  blob.resize(off + std::max<size_t>(v.size() * sizeof(T), 1));
+  if (!v.empty()) std::memcpy(blob.data() + off, v.data(), v.size() * sizeof(T));
+  return off;
+}
+
+epic_status upload(epic_ctx* c) {
+  const HostTables& H = c->H;
+  std::vector<char> blob;
+  size_t o_trans = place(blob, H.trans), o_accept = place(blob, H.accept), o_ext = place(blob, H.ext),
+         o_flush = place(blob, H.flushlab), o_cexit = place(blob, H.cls_exit), o_cint = place(blob, H.cls_internal),
+         o_centry = place(blob, H.cls_entry), o_cflush = place(blob, H.cls_flush), o_expt = place(blob, H.exp_t),
+         o_expn = place(blob, H.exp_n), o_pred = place(blob, H.pred), o_comp = place(blob, H.complete),
+         o_lhs = place(blob, H.item_lhs), o_nnt = place(blob, H.next_nt), o_ccl = place(blob, H.cover_cl),
+         o_vb = place(blob, H.vbytes), o_vo = place(blob, H.voffs);
+  if (hipMalloc(&c->d_tables, blob.size()) != hipSuccess) return EPIC_ERR_HIP;
+  if (hipMemcpy(c->d_tables, blob.data(), blob.size(), hipMemcpyHostToDevice) != hipSuccess) return EPIC_ERR_HIP;
+  if (hipMalloc((void**)&c->d_memo, (size_t)H.V * H.Q * sizeof(uint4)) != hipSuccess) return EPIC_ERR_HIP;
+  if (hipMalloc((void**)&c->d_err, 256) != hipSuccess) return EPIC_ERR_HIP;
+  if (hipMemset(c->d_err, 0, 256) != hipSuccess) return EPIC_ERR_HIP;
+  char* d = (char*)c->d_tables;
+  DevTab& t = c->tab;
+  t.Q = H.Q;
+  t.T = H.T;
+  t.N = H.N;
+  t.NI = H.NI;
+  t.W = H.W;
+  t.CW = H.CW;
+  t.K = H.K;
+  t.QW = H.QW;
+  t.V = H.V;
+  t.start_nt = H.start_nt;
+  t.start_item = H.start_item;
+  t.goal_item = H.goal_item;
+  t.trans = (const int16_t*)(d + o_trans);
+  t.accept = (const int16_t*)(d + o_accept);
+  t.ext = (const uint32_t*)(d + o_ext);
+  t.flushlab = (const uint64_t*)(d + o_flush);
+  t.cls_exit = (const uint32_t*)(d + o_cexit);
+  t.cls_internal = (const uint64_t*)(d + o_cint);
+  t.cls_entry = (const uint64_t*)(d + o_centry);
+  t.cls_flush = (const uint64_t*)(d + o_cflush);
+  t.exp_t = (const uint32_t*)(d + o_expt);
+  t.exp_n = (const uint32_t*)(d + o_expn);
+  t.pred = (const uint32_t*)(d + o_pred);
+  t.complete = (const uint32_t*)(d + o_comp);
+  t.item_lhs = (const int8_t*)(d + o_lhs);
+  t.next_nt = (const int8_t*)(d + o_nnt);
+  t.cover_cl = (const uint32_t*)(d + o_ccl);
+  t.vbytes = (const uint8_t*)(d + o_vb);
+  t.voffs = (const int32_t*)(d + o_vo);
+  t.memo = c->d_memo;
+  t.dev_err = c->d_err;
+  return EPIC_OK;
+}
+
+WsArgs ws_args(const epic_ctx* c, void* ws) {
+  WsArgs a;
+  a.base = (char*)ws;
+  a.slot_bytes = c->slot_bytes;
+  a.off_cnt = c->off_cnt;
+  a.off_org = c->off_org;
+  a.off_sum = c->off_sum;
+  a.off_bits = c->off_bits;
+  a.off_cov = c->off_cov;
+  a.off_tqn = c->off_tqn;
+  a.off_tqm = c->off_tqm;
+  a.maxn = c->maxn;
+  a.maxe = c->maxe;
+  a.tcap = c->tcap;
+  return a;
+}
+
+template <template <int> class Launcher, class... Args>
+epic_status dispatch_w(int W, Args... args) {
+  switch (W) {
+    case 1: return Launcher<1>::run(args...);
+    case 2: return Launcher<2>::run(args...);
+    case 4: return Launcher<4>::run(args...);
+    case 8: return Launcher<8>::run(args...);
+    case 16: return Launcher<16>::run(args...);
+    default: return EPIC_ERR_UNSUPPORTED;
+  }
+}
+
+template <int W>
+struct ValidateLaunch {
+  static epic_status run(epic_ctx* c, const int32_t* seqs, int B, int n, const int32_t* cs, const int32_t* cp,
+                         const int32_t* ct, int C, uint8_t* verdict, void* ws, hipStream_t stream) {
+    int grid = std::min(C, c->nslot);
+    hipLaunchKernelGGL((validate_kernel<W>), dim3(grid), dim3(kThreads), 0, stream, c->tab, seqs, B, n, cs, cp, ct,
+                       C, verdict, ws_args(c, ws));
+    return hipGetLastError() == hipSuccess ? EPIC_OK : EPIC_ERR_HIP;
+  }
+};
+
+template <int W>
+struct SelectLaunch {
+  static epic_status run(epic_ctx* c, const int32_t* seqs, int B, int n, const int32_t* cs, const int32_t* cp,
+                         const int32_t* ct, const float* conf, const uint8_t* verdict, int C, uint8_t* sel,
+                         int64_t* counts, void* ws, hipStream_t stream) {
+    hipLaunchKernelGGL((select_kernel<W>), dim3(B), dim3(kThreads), 0, stream, c->tab, seqs, B, n, cs, cp, ct, conf,
+                       verdict, C, sel, (long long*)counts, ws_args(c, ws));
+    return hipGetLastError() == hipSuccess ? EPIC_OK : EPIC_ERR_HIP;
+  }
+};
+
+}  // namespace
+
+extern "C" {
+
+const char* epic_status_string(epic_status s) {
+  switch (s) {
+    case EPIC_OK: return "ok";
+    case EPIC_ERR_NULL: return "null pointer";
+    case EPIC_ERR_ARG: return "argument out of range";
+    case EPIC_ERR_CAPACITY: return "capacity exceeded";
+    case EPIC_ERR_LEXER: return "malformed lexer DFA";
+    case EPIC_ERR_GRAMMAR: return "malformed grammar";
+    case EPIC_ERR_VOCAB: return "malformed vocabulary";
+    case EPIC_ERR_HIP: return "HIP runtime error";
+    case EPIC_ERR_STATE: return "memo not built";
+    case EPIC_ERR_UNSUPPORTED: return "unsupported size";
+  }
+  return "unknown status";
+}
+
+epic_status epic_ctx_create(const epic_lexer_desc* lexer, const epic_grammar_desc* grammar,
+                            const epic_vocab_desc* vocab, int32_t max_batch, int32_t max_seq_len, int32_t max_cands,
+                            epic_ctx** out) {
+  if (!lexer || !grammar || !vocab || !out || !lexer->trans || !lexer->accept || !grammar->lhs ||
+      !grammar->rhs_offsets || !vocab->bytes || !vocab->offsets)
+    return EPIC_ERR_NULL;
+  if (grammar->num_productions > 0 && grammar->rhs_offsets[grammar->num_productions] > 0 && !grammar->rhs)
+    return EPIC_ERR_NULL;
+  *out = nullptr;
+  if (max_batch < 1 || max_seq_len < 1 || max_cands < 1) return EPIC_ERR_ARG;
+  if (max_seq_len > kMaxSeq) return EPIC_ERR_UNSUPPORTED;
+  epic_ctx* c = new epic_ctx();
+  std::string why;
+  int r = build_tables(lexer->num_states, lexer->trans, lexer->accept, grammar->num_terminals,
+                       grammar->num_nonterminals, grammar->start, grammar->num_productions, grammar->lhs,
+                       grammar->rhs_offsets, grammar->rhs, vocab->vocab_size, vocab->bytes, vocab->offsets, c->H, why);
+  if (r != 0) {
+    delete c;
+    return (epic_status)r;
+  }
+  if (hipGetDevice(&c->device) != hipSuccess) c->device = 0;
+  c->max_batch = max_batch;
+  c->max_seq = max_seq_len;
+  c->max_cands = max_cands;
+  const HostTables& H = c->H;
+  // graph nodes: start, final, one per fixed byte, K per masked run
+  c->maxn = 8 * max_seq_len + H.K * (max_seq_len / 2 + 2) + 4;
+  c->maxe = std::max(16384, 256 * max_seq_len);
+  c->tcap = 16384;
+  c->nslot = std::min(std::max(max_cands, max_batch), 1024);
+  c->off_cnt = align256((size_t)c->maxn * 4);
+  c->off_org = c->off_cnt + align256((size_t)c->maxn * 4);
+  c->off_sum = c->off_org + align256((size_t)c->maxe * 2);
+  c->off_bits = c->off_sum + align256((size_t)c->maxe * 8);
+  c->off_cov = c->off_bits + align256((size_t)c->maxe * H.W * 4);
+  c->off_tqn = c->off_cov + align256((size_t)c->maxn * H.CW * 4);
+  c->off_tqm = c->off_tqn + align256((size_t)2 * c->tcap * 4);
+  c->slot_bytes = c->off_tqm + align256((size_t)2 * c->tcap * 8);
+  c->ws_bytes = c->slot_bytes * c->nslot;
+  epic_status s = upload(c);
+  if (s != EPIC_OK) {
+    epic_ctx_destroy(c);
+    return s;
+  }
+  *out = c;
+  return EPIC_OK;
+}
+
+void epic_ctx_destroy(epic_ctx* c) {
+  if (!c) return;
+  if (c->d_tables) (void)hipFree(c->d_tables);
+  if (c->d_memo) (void)hipFree(c->d_memo);
+  if (c->d_err) (void)hipFree(c->d_err);
+  delete c;
+}
+
+size_t epic_workspace_bytes(const epic_ctx* c) { return c ? c->ws_bytes : 0; }
+
+int32_t epic_gap_classes(const epic_ctx* c) { return c ? c->H.K : -1; }
+
+epic_status epic_lexmemo_build(epic_ctx* c, hipStream_t stream) {
+  if (!c) return EPIC_ERR_NULL;
+  const size_t total = (size_t)c->H.V * c->H.Q;
+  const unsigned grid = (unsigned)((total + kThreads - 1) / kThreads);
+  hipLaunchKernelGGL(lexmemo_kernel, dim3(grid), dim3(kThreads), 0, stream, c->tab, c->d_memo);
+  if (hipGetLastError() != hipSuccess) return EPIC_ERR_HIP;
+  c->memo_built = true;
+  return EPIC_OK;
+}
+
+epic_status epic_memo_export(const epic_ctx* c, void* host_dst, size_t bytes) {
+  if (!c || !host_dst) return EPIC_ERR_NULL;
+  if (!c->memo_built) return EPIC_ERR_STATE;
+  const size_t need = (size_t)c->H.V * c->H.Q * 16;
+  if (bytes < need) return EPIC_ERR_CAPACITY;
+  if (hipDeviceSynchronize() != hipSuccess) return EPIC_ERR_HIP;
+  if (hipMemcpy(host_dst, c->d_memo, need, hipMemcpyDeviceToHost) != hipSuccess) return EPIC_ERR_HIP;
+  return EPIC_OK;
+}
+
+static epic_status check_batch(const epic_ctx* c, const int32_t* seqs, int B, int n, const int32_t* cs,
+                               const int32_t* cp, const int32_t* ct, int C, const void* out, const void* ws,
+                               size_t ws_bytes) {
+  if (!c) return EPIC_ERR_NULL;
+  if (B < 0 || n < 0 || C < 0) return EPIC_ERR_ARG;
+  if (B > c->max_batch || n > c->max_seq || C > c->max_cands) return EPIC_ERR_CAPACITY;
+  if (C == 0) return EPIC_OK;
+  if (!seqs || !cs || !cp || !ct || !out || !ws) return EPIC_ERR_NULL;
+  if (((uintptr_t)ws & 255) != 0) return EPIC_ERR_ARG;
+  if (ws_bytes < c->ws_bytes) return EPIC_ERR_CAPACITY;
+  if (!c->memo_built) return EPIC_ERR_STATE;
+  return EPIC_OK;
+}
+
+epic_status epic_validate_batch(epic_ctx* c, const int32_t* d_seqs, int32_t B, int32_t n, const int32_t* d_cand_seq,
+                                const int32_t* d_cand_pos, const int32_t* d_cand_tok, int32_t C, uint8_t* d_verdict,
+                                void* d_workspace, size_t workspace_bytes, hipStream_t stream) {
+  epic_status s =
+      check_batch(c, d_seqs, B, n, d_cand_seq, d_cand_pos, d_cand_tok, C, d_verdict, d_workspace, workspace_bytes);
+  if (s != EPIC_OK || C == 0) return s;
+  return dispatch_w<ValidateLaunch>(c->H.W, c, d_seqs, (int)B, (int)n, d_cand_seq, d_cand_pos, d_cand_tok, (int)C,
+                                    d_verdict, d_workspace, stream);
+}
+
+epic_status epic_select_compatible(epic_ctx* c, const int32_t* d_seqs, int32_t B, int32_t n,
+                                   const int32_t* d_cand_seq, const int32_t* d_cand_pos, const int32_t* d_cand_tok,
+                                   const float* d_conf, const uint8_t* d_verdict, int32_t C, uint8_t* d_selected,
+                                   int64_t* d_counts, void* d_workspace, size_t workspace_bytes, hipStream_t stream) {
+  epic_status s =
+      check_batch(c, d_seqs, B, n, d_cand_seq, d_cand_pos, d_cand_tok, C, d_selected, d_workspace, workspace_bytes);
+  if (s != EPIC_OK || C == 0 || B == 0) return s;
+  if (!d_conf || !d_verdict) return EPIC_ERR_NULL;
+  if (B > c->nslot) return EPIC_ERR_CAPACITY;
+  return dispatch_w<SelectLaunch>(c->H.W, c, d_seqs, (int)B, (int)n, d_cand_seq, d_cand_pos, d_cand_tok, d_conf,
+                                  d_verdict, (int)C, d_selected, d_counts, d_workspace, stream);
+}
+
+epic_status epic_ctx_device_error(epic_ctx* c, hipStream_t stream, uint32_t* flags) {
+  if (!c || !flags) return EPIC_ERR_NULL;
+  if (hipStreamSynchronize(stream) != hipSuccess) return EPIC_ERR_HIP;
+  uint32_t v = 0;
+  if (hipMemcpy(&v, c->d_err, 4, hipMemcpyDeviceToHost) != hipSuccess) return EPIC_ERR_HIP;
+  if (hipMemset(c->d_err, 0, 4) != hipSuccess) return EPIC_ERR_HIP;
+  *flags = v;
+  return EPIC_OK;
+}
+
+}  // extern "C"

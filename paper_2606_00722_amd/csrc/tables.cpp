@@ -1,0 +1,402 @@
+// Host-side constant tables of the HIP path.
+//
+// Everything here depends only on the lexer, the grammar and the vocabulary,
+// never on a sequence; it is computed once when a context is created.
+//
+//  * Dotted items, numbered consecutively per production so that advancing
+//    the dot is a one-bit left shift of an item bitset; the augmented
+//    production S' -> S comes last.  Prediction tables use the left-corner
+//    closure (Alg. 3's predict step applied until nothing new appears;
+//    nullable prefixes are left to completion at run time).
+//  * The lexer's gap automaton.  A masked run reads Sigma* (Limitations), so
+//    inside it a lexeme extends along any byte, and a lexeme ends on a byte
+//    that cannot extend it but starts a new one.  The lexeme-level nodes of a
+//    gap are the "fresh" states delta(q0, c) reached right after an emission.
+//    Fresh states with the same left language for every state in which the
+//    gap can be entered are merged (exactly: their membership in every subset
+//    of the gap automaton's determinisation, over all entry states, agrees).
+//    Merging nodes with equal left languages keeps the language of the
+//    completion automaton, so Valid is unchanged.  For lexers where whitespace
+//    can separate any two lexemes this leaves one class per gap.
+//  * The regular cover of App. A.2: its rule-position states are the dotted
+//    items; entry/exit states of each nonterminal are extra bits.
+#include "tables.h"
+
+#include <algorithm>
+#include <map>
+#include <set>
+#include <vector>
+
+#include "../../include/epic.h"
+
+namespace epic {
+namespace {
+
+struct Bits {
+  std::vector<uint64_t> w;
+  explicit Bits(int n = 0) : w((n + 63) / 64, 0) {}
+  void set(int i) { w[i >> 6] |= 1ull << (i & 63); }
+  bool get(int i) const { return (w[i >> 6] >> (i & 63)) & 1; }
+  bool any() const {
+    for (uint64_t x : w)
+      if (x) return true;
+    return false;
+  }
+  bool operator<(const Bits& o) const { return w < o.w; }
+  bool operator==(const Bits& o) const { return w == o.w; }
+};
+
+inline void set32(std::vector<uint32_t>& v, size_t base, int i) { v[base + (i >> 5)] |= 1u << (i & 31); }
+
+}  // namespace
+
+int build_tables(int Q, const int16_t* trans, const int16_t* accept, int T, int N, int start, int P,
+                 const int32_t* lhs, const int32_t* roff, const int32_t* rhs, int V, const uint8_t* vbytes,
+                 const int32_t* voffs, HostTables& H, std::string& why) {
+  // ---------------------------------------------------------------- checks
+  if (T < 1 || T > kMaxTerminals || N < 1 || N > kMaxNonterminals) {
+    why = "grammar has too many terminals or nonterminals";
+    return EPIC_ERR_UNSUPPORTED;
+  }
+  if (Q < 1 || Q > kMaxStates) {
+    why = "lexer has too many states";
+    return EPIC_ERR_UNSUPPORTED;
+  }
+  if (accept[0] != -1) {
+    why = "lexer start state accepts";
+    return EPIC_ERR_LEXER;
+  }
+  for (int q = 0; q < Q; ++q) {
+    int a = accept[q];
+    if (!(a == -1 || a == -2 || (a >= 0 && a < T))) {
+      why = "lexer accept label out of range";
+      return EPIC_ERR_LEXER;
+    }
+    for (int c = 0; c < 256; ++c)
+      if (trans[q * 256 + c] < -1 || trans[q * 256 + c] >= Q) {
+        why = "lexer transition out of range";
+        return EPIC_ERR_LEXER;
+      }
+  }
+  {  // trim: every state reaches an accepting state
+    std::vector<char> live(Q, 0);
+    for (int q = 0; q < Q; ++q) live[q] = accept[q] != -1;
+    bool changed = true;
+    while (changed) {
+      changed = false;
+      for (int q = 0; q < Q; ++q)
+        if (!live[q])
+          for (int c = 0; c < 256; ++c) {
+            int d = trans[q * 256 + c];
+            if (d >= 0 && live[d]) {
+              live[q] = 1;
+              changed = true;
+              break;
+            }
+          }
+    }
+    for (int q = 0; q < Q; ++q)
+      if (!live[q]) {
+        why = "lexer DFA is not trim";
+        return EPIC_ERR_LEXER;
+      }
+  }
+  if (P < 1 || start < T || start >= T + N || roff[0] != 0) {
+    why = "bad grammar header";
+    return EPIC_ERR_GRAMMAR;
+  }
+  for (int p = 0; p < P; ++p) {
+    if (lhs[p] < T || lhs[p] >= T + N || roff[p + 1] < roff[p]) {
+      why = "bad production";
+      return EPIC_ERR_GRAMMAR;
+    }
+    for (int k = roff[p]; k < roff[p + 1]; ++k)
+      if (rhs[k] < 0 || rhs[k] >= T + N) {
+        why = "undefined symbol";
+        return EPIC_ERR_GRAMMAR;
+      }
+  }
+  if (V < 1) {
+    why = "empty vocabulary";
+    return EPIC_ERR_VOCAB;
+  }
+  for (int t = 0; t < V; ++t) {
+    int len = voffs[t + 1] - voffs[t];
+    if (len < 1 || len > 8) {
+      why = "token length must be 1..8 bytes";
+      return EPIC_ERR_VOCAB;
+    }
+  }
+
+  H = HostTables();
+  H.Q = Q;
+  H.T = T;
+  H.N = N;
+  H.P = P;
+  H.V = V;
+  H.QW = (Q + 31) / 32;
+  H.trans.assign(trans, trans + (size_t)Q * 256);
+  H.accept.assign(accept, accept + Q);
+  H.vbytes.assign(vbytes, vbytes + voffs[V]);
+  if (H.vbytes.empty()) H.vbytes.push_back(0);
+  H.voffs.assign(voffs, voffs + V + 1);
+
+  // ---------------------------------------------------------------- items
+  std::vector<int> base(P + 1);
+  int ni = 0;
+  for (int p = 0; p < P; ++p) {
+    base[p] = ni;
+    int len = roff[p + 1] - roff[p];
+    ni += len + 1;
+    H.max_rhs = std::max(H.max_rhs, len);
+  }
+  base[P] = ni;
+  ni += 2;  // S' -> . S and S' -> S .
+  H.max_rhs = std::max(H.max_rhs, 1);
+  H.NI = ni;
+  int words = (ni + 31) / 32;
+  int W = 1;
+  while (W < words) W *= 2;
+  if (W > kMaxItemWords) {
+    why = "more than 512 dotted items";
+    return EPIC_ERR_UNSUPPORTED;
+  }
+  H.W = W;
+  H.CW = W + 4;  // cover state: items, then entry bits (2 words), then exit bits (2 words)
+  H.start_nt = start - T;
+  H.start_item = base[P];
+  H.goal_item = base[P] + 1;
+  H.exp_t.assign((size_t)T * W, 0);
+  H.exp_n.assign((size_t)N * W, 0);
+  H.pred.assign((size_t)N * W, 0);
+  H.complete.assign(W, 0);
+  H.item_lhs.assign(ni, -1);
+  H.next_nt.assign(ni, -1);
+  H.start_of.assign((size_t)N * W, 0);
+  H.end_of.assign((size_t)N * W, 0);
+  for (int p = 0; p <= P; ++p) {
+    int len = p < P ? roff[p + 1] - roff[p] : 1;
+    int A = p < P ? lhs[p] - T : -1;
+    for (int k = 0; k <= len; ++k) {
+      int it = base[p] + k;
+      H.item_lhs[it] = (int8_t)A;
+      if (k < len) {
+        int X = p < P ? rhs[roff[p] + k] : start;
+        if (X < T) {
+          set32(H.exp_t, (size_t)X * W, it);
+        } else {
+          set32(H.exp_n, (size_t)(X - T) * W, it);
+          H.next_nt[it] = (int8_t)(X - T);
+        }
+      } else if (p < P) {
+        set32(H.complete, 0, it);
+      }
+    }
+    if (p < P) {
+      set32(H.start_of, (size_t)A * W, base[p]);
+      set32(H.end_of, (size_t)A * W, base[p] + len);
+    }
+  }
+  for (int B = 0; B < N; ++B) {  // left-corner closure
+    std::vector<char> in(N, 0);
+    in[B] = 1;
+    bool changed = true;
+    while (changed) {
+      changed = false;
+      for (int p = 0; p < P; ++p) {
+        int A = lhs[p] - T;
+        if (!in[A] || roff[p + 1] == roff[p]) continue;
+        int X = rhs[roff[p]];
+        if (X >= T && !in[X - T]) {
+          in[X - T] = 1;
+          changed = true;
+        }
+      }
+    }
+    for (int p = 0; p < P; ++p)
+      if (in[lhs[p] - T]) set32(H.pred, (size_t)B * W, base[p]);
+  }
+
+  // ---------------------------------------------------------------- cover
+  {
+    // epsilon edges of the flattened recursive transition network (App. A.2):
+    // entry_A -> (p,0) for A's productions, (p,|rhs|) -> exit_A, a nonterminal
+    // B at (p,k): (p,k) -> entry_B and exit_B -> (p,k+1) for every occurrence
+    const int CW = H.CW, nbits = CW * 32;
+    auto ENT = [&](int A) { return W * 32 + A; };
+    auto EXT = [&](int A) { return W * 32 + 64 + A; };
+    std::vector<std::vector<int>> eps(nbits);
+    for (int p = 0; p < P; ++p) {
+      int A = lhs[p] - T, len = roff[p + 1] - roff[p];
+      eps[ENT(A)].push_back(base[p]);
+      eps[base[p] + len].push_back(EXT(A));
+      for (int k = 0; k < len; ++k) {
+        int X = rhs[roff[p] + k];
+        if (X >= T) {
+          eps[base[p] + k].push_back(ENT(X - T));
+          eps[EXT(X - T)].push_back(base[p] + k + 1);
+        }
+      }
+    }
+    H.cover_cl.assign((size_t)nbits * CW, 0);
+    for (int s = 0; s < nbits; ++s) {
+      std::vector<char> seen(nbits, 0);
+      std::vector<int> st{s};
+      seen[s] = 1;
+      while (!st.empty()) {
+        int u = st.back();
+        st.pop_back();
+        set32(H.cover_cl, (size_t)s * CW, u);
+        for (int v : eps[u])
+          if (!seen[v]) {
+            seen[v] = 1;
+            st.push_back(v);
+          }
+      }
+    }
+  }
+
+  // ---------------------------------------------------------------- lexer
+  const int QW = H.QW;
+  H.ext.assign((size_t)Q * QW, 0);
+  for (int q = 0; q < Q; ++q) {
+    std::vector<char> seen(Q, 0);
+    std::vector<int> st{q};
+    seen[q] = 1;
+    while (!st.empty()) {
+      int u = st.back();
+      st.pop_back();
+      set32(H.ext, (size_t)q * QW, u);
+      for (int c = 0; c < 256; ++c) {
+        int d = trans[u * 256 + c];
+        if (d >= 0 && !seen[d]) {
+          seen[d] = 1;
+          st.push_back(d);
+        }
+      }
+    }
+  }
+  H.flushlab.assign(Q, 0);
+  for (int q = 0; q < Q; ++q) {
+    if (q == 0 || accept[q] == -2)
+      H.flushlab[q] = 1ull << kLabelEps;
+    else if (accept[q] >= 0)
+      H.flushlab[q] = 1ull << accept[q];
+  }
+  // fresh states and emissions
+  std::vector<int> fresh_id(Q, -1), fresh;
+  for (int c = 0; c < 256; ++c) {
+    int f = trans[c];
+    if (f >= 0 && fresh_id[f] < 0) {
+      fresh_id[f] = (int)fresh.size();
+      fresh.push_back(f);
+    }
+  }
+  const int F = (int)fresh.size();
+  // emit[q][r] = labels emitted when a lexeme ending in state q is followed by
+  // a byte that starts fresh state r
+  std::vector<std::vector<uint64_t>> emit(Q, std::vector<uint64_t>(F, 0));
+  for (int q = 0; q < Q; ++q) {
+    if (accept[q] == -1) continue;
+    uint64_t lab = accept[q] == -2 ? (1ull << kLabelEps) : (1ull << accept[q]);
+    for (int c = 0; c < 256; ++c)
+      if (trans[q * 256 + c] < 0 && trans[c] >= 0) emit[q][fresh_id[trans[c]]] |= lab;
+  }
+  auto in_ext = [&](int q, int u) { return (H.ext[(size_t)q * QW + (u >> 5)] >> (u & 31)) & 1; };
+  std::vector<std::vector<uint64_t>> internal(F, std::vector<uint64_t>(F, 0));
+  for (int r = 0; r < F; ++r)
+    for (int q = 0; q < Q; ++q)
+      if (in_ext(fresh[r], q))
+        for (int r2 = 0; r2 < F; ++r2) internal[r][r2] |= emit[q][r2];
+  std::vector<std::vector<uint64_t>> entry(Q, std::vector<uint64_t>(F, 0));
+  for (int qi = 0; qi < Q; ++qi)
+    for (int q = 0; q < Q; ++q)
+      if (in_ext(qi, q))
+        for (int r2 = 0; r2 < F; ++r2) entry[qi][r2] |= emit[q][r2];
+  // left-language classes: determinise from every entry state, record subsets
+  auto closure = [&](Bits s) {
+    bool changed = true;
+    while (changed) {
+      changed = false;
+      for (int r = 0; r < F; ++r)
+        if (s.get(r))
+          for (int r2 = 0; r2 < F; ++r2)
+            if (!s.get(r2) && ((internal[r][r2] >> kLabelEps) & 1)) {
+              s.set(r2);
+              changed = true;
+            }
+    }
+    return s;
+  };
+  std::map<Bits, int> subsets;
+  for (int qi = 0; qi < Q; ++qi) {
+    Bits s0(F);
+    for (int r = 0; r < F; ++r)
+      if ((entry[qi][r] >> kLabelEps) & 1) s0.set(r);
+    s0 = closure(s0);
+    std::set<Bits> seen;
+    std::vector<std::pair<bool, Bits>> work{{true, s0}};
+    if (s0.any()) subsets.emplace(s0, (int)subsets.size());
+    std::set<std::pair<bool, Bits>> visited{{true, s0}};
+    for (size_t i = 0; i < work.size(); ++i) {
+      bool from_entry = work[i].first;
+      Bits cur = work[i].second;
+      for (int a = 0; a < T; ++a) {
+        Bits nx(F);
+        for (int r2 = 0; r2 < F; ++r2) {
+          bool hit = from_entry && ((entry[qi][r2] >> a) & 1);
+          for (int r = 0; r < F && !hit; ++r)
+            if (cur.get(r) && ((internal[r][r2] >> a) & 1)) hit = true;
+          if (hit) nx.set(r2);
+        }
+        if (!nx.any()) continue;
+        nx = closure(nx);
+        if (visited.insert({false, nx}).second) {
+          work.push_back({false, nx});
+          if (!subsets.count(nx)) subsets.emplace(nx, (int)subsets.size());
+        }
+      }
+    }
+  }
+  std::map<std::vector<int>, int> sig2class;
+  std::vector<int> cls_of(F, -1);
+  for (int r = 0; r < F; ++r) {
+    std::vector<int> sig;
+    for (auto& kv : subsets)
+      if (kv.first.get(r)) sig.push_back(kv.second);
+    if (sig.empty()) continue;  // never reached inside a gap
+    std::sort(sig.begin(), sig.end());
+    auto it = sig2class.find(sig);
+    if (it == sig2class.end()) {
+      int k = (int)sig2class.size();
+      sig2class[sig] = k;
+      cls_of[r] = k;
+    } else {
+      cls_of[r] = it->second;
+    }
+  }
+  const int K = (int)sig2class.size();
+  if (K > kMaxGapClasses) {
+    why = "lexer gap automaton has too many left-language classes";
+    return EPIC_ERR_UNSUPPORTED;
+  }
+  H.K = K;
+  H.cls_exit.assign((size_t)std::max(K, 1) * QW, 0);
+  H.cls_internal.assign((size_t)std::max(K * K, 1), 0);
+  H.cls_entry.assign((size_t)Q * std::max(K, 1), 0);
+  H.cls_flush.assign(std::max(K, 1), 0);
+  for (int r = 0; r < F; ++r) {
+    int k = cls_of[r];
+    if (k < 0) continue;
+    for (int w = 0; w < QW; ++w) H.cls_exit[(size_t)k * QW + w] |= H.ext[(size_t)fresh[r] * QW + w];
+    for (int r2 = 0; r2 < F; ++r2)
+      if (cls_of[r2] >= 0) H.cls_internal[(size_t)k * K + cls_of[r2]] |= internal[r][r2];
+    for (int qi = 0; qi < Q; ++qi) H.cls_entry[(size_t)qi * K + k] |= entry[qi][r];
+  }
+  for (int k = 0; k < K; ++k)
+    for (int q = 0; q < Q; ++q)
+      if ((H.cls_exit[(size_t)k * QW + (q >> 5)] >> (q & 31)) & 1) H.cls_flush[k] |= H.flushlab[q];
+  return 0;
+}
+
+}  // namespace epic

@@ -1,0 +1,57 @@
+// Host-side constant tables of the HIP path (built once per context).
+#pragma once
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+namespace epic {
+
+constexpr int kLabelEps = 63;  // bit 63 of a 64-bit label set = epsilon (skip lexeme)
+constexpr int kMaxTerminals = 63;
+constexpr int kMaxNonterminals = 64;
+constexpr int kMaxStates = 256;
+constexpr int kMaxItemWords = 16;  // 512 dotted items
+constexpr int kMaxGapClasses = 8;
+
+struct HostTables {
+  // sizes
+  int Q = 0, T = 0, N = 0, P = 0, NI = 0, W = 0, CW = 0, K = 0, QW = 0, V = 0;
+  int start_nt = 0;    // nonterminal index (0..N-1) of the start symbol
+  int start_item = 0;  // S' -> . S
+  int goal_item = 0;   // S' -> S .
+  int max_rhs = 0;
+  // lexer
+  std::vector<int16_t> trans;     // [Q*256]
+  std::vector<int16_t> accept;    // [Q]
+  std::vector<uint32_t> ext;      // [Q*QW] states reachable from q without an emission (q included)
+  std::vector<uint64_t> flushlab; // [Q] label set of flushing state q (empty = dies)
+  // gap automaton, reduced to left-language classes
+  std::vector<uint32_t> cls_exit;       // [K*QW] lexer states in which a gap may end inside class k
+  std::vector<uint64_t> cls_internal;   // [K*K] labels of edges class k -> class k'
+  std::vector<uint64_t> cls_entry;      // [Q*K] labels of edges from an entry lexeme in state q into class k
+  std::vector<uint64_t> cls_flush;      // [K]
+  // grammar (dotted items numbered per production, consecutively)
+  std::vector<uint32_t> exp_t;     // [T*W] items whose next symbol is terminal a
+  std::vector<uint32_t> exp_n;     // [N*W] items whose next symbol is nonterminal B
+  std::vector<uint32_t> pred;      // [N*W] items B' -> . gamma for B' in the left-corner closure of B
+  std::vector<uint32_t> complete;  // [W] items with the dot at the end (augmented item excluded)
+  std::vector<int8_t> item_lhs;    // [NI] nonterminal index of the item's production (-1: augmented)
+  std::vector<int8_t> next_nt;     // [NI] nonterminal index after the dot (-1: terminal or end)
+  std::vector<uint32_t> start_of;  // [N*W] items A -> . gamma
+  std::vector<uint32_t> end_of;    // [N*W] items A -> gamma .
+  // regular cover: state bit i < 32W is dotted item i (rule position), bit 32W+A is
+  // the entry state of nonterminal A, bit 32W+64+A its exit state; cover_cl[s] is
+  // the epsilon closure of state s (row of CW words, 32*CW rows)
+  std::vector<uint32_t> cover_cl;
+  // vocabulary
+  std::vector<uint8_t> vbytes;
+  std::vector<int32_t> voffs;
+};
+
+// Returns 0 or an epic_status error code; `why` receives a message.
+int build_tables(int Q, const int16_t* trans, const int16_t* accept, int T, int N, int start, int P,
+                 const int32_t* lhs, const int32_t* roff, const int32_t* rhs, int V, const uint8_t* vbytes,
+                 const int32_t* voffs, HostTables& out, std::string& why);
+
+}  // namespace epic

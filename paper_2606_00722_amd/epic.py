@@ -1,0 +1,183 @@
+"""Python binding of the C ABI in include/epic.h (argument marshalling only).
+
+Device buffers are PyTorch tensors on a HIP device; every call enqueues on the
+given torch stream (default: the current stream).  All computation happens in
+the HIP kernels of libepic.so; there is no fallback: if the library is not
+built, loading it raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libepic.so")
+
+STATUS = {0: "ok", -1: "null pointer", -2: "argument out of range", -3: "capacity exceeded",
+          -4: "malformed lexer DFA", -5: "malformed grammar", -6: "malformed vocabulary",
+          -7: "HIP runtime error", -8: "memo not built", -9: "unsupported size"}
+DEV_BAD_CANDIDATE, DEV_CAPACITY, DEV_BAD_SELECT = 1, 2, 4
+
+FUNCTIONS = ["epic_ctx_create", "epic_ctx_destroy", "epic_workspace_bytes", "epic_gap_classes",
+             "epic_lexmemo_build", "epic_memo_export", "epic_validate_batch", "epic_select_compatible",
+             "epic_ctx_device_error", "epic_status_string"]
+
+
+class EpicError(RuntimeError):
+    def __init__(self, fn: str, code: int):
+        super().__init__(f"{fn}: {STATUS.get(code, code)} ({code})")
+        self.code = code
+
+
+class _Lexer(ctypes.Structure):
+    _fields_ = [("num_states", ctypes.c_int32), ("trans", ctypes.c_void_p), ("accept", ctypes.c_void_p)]
+
+
+class _Grammar(ctypes.Structure):
+    _fields_ = [("num_terminals", ctypes.c_int32), ("num_nonterminals", ctypes.c_int32),
+                ("start", ctypes.c_int32), ("num_productions", ctypes.c_int32),
+                ("lhs", ctypes.c_void_p), ("rhs_offsets", ctypes.c_void_p), ("rhs", ctypes.c_void_p)]
+
+
+class _Vocab(ctypes.Structure):
+    _fields_ = [("vocab_size", ctypes.c_int32), ("bytes", ctypes.c_void_p), ("offsets", ctypes.c_void_p)]
+
+
+_lib: Optional[ctypes.CDLL] = None
+
+
+def lib() -> ctypes.CDLL:
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"libepic.so is not built ({LIB_PATH}); run __graft_entry__.build()")
+        L = ctypes.CDLL(LIB_PATH)
+        P, i32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+        L.epic_ctx_create.argtypes = [P, P, P, i32, i32, i32, ctypes.POINTER(P)]
+        L.epic_ctx_create.restype = ctypes.c_int
+        L.epic_ctx_destroy.argtypes = [P]
+        L.epic_ctx_destroy.restype = None
+        L.epic_workspace_bytes.argtypes = [P]
+        L.epic_workspace_bytes.restype = sz
+        L.epic_gap_classes.argtypes = [P]
+        L.epic_gap_classes.restype = i32
+        L.epic_lexmemo_build.argtypes = [P, P]
+        L.epic_lexmemo_build.restype = ctypes.c_int
+        L.epic_memo_export.argtypes = [P, P, sz]
+        L.epic_memo_export.restype = ctypes.c_int
+        L.epic_validate_batch.argtypes = [P, P, i32, i32, P, P, P, i32, P, P, sz, P]
+        L.epic_validate_batch.restype = ctypes.c_int
+        L.epic_select_compatible.argtypes = [P, P, i32, i32, P, P, P, P, P, i32, P, P, P, sz, P]
+        L.epic_select_compatible.restype = ctypes.c_int
+        L.epic_ctx_device_error.argtypes = [P, P, ctypes.POINTER(ctypes.c_uint32)]
+        L.epic_ctx_device_error.restype = ctypes.c_int
+        L.epic_status_string.argtypes = [ctypes.c_int]
+        L.epic_status_string.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+def _check(fn: str, code: int):
+    if code != 0:
+        raise EpicError(fn, code)
+
+
+def _ptr(t) -> int:
+    return 0 if t is None else int(t.data_ptr())
+
+
+def _stream(stream) -> int:
+    import torch
+
+    s = torch.cuda.current_stream() if stream is None else stream
+    return int(s.cuda_stream)
+
+
+class Context:
+    """An epic_ctx: lexer DFA, grammar and vocabulary tables on the device."""
+
+    def __init__(self, trans, accept, num_terminals, num_nonterminals, start, lhs, rhs_offsets, rhs,
+                 vocab_bytes, vocab_offsets, max_batch, max_seq_len, max_cands):
+        self._keep = [np.ascontiguousarray(trans, np.int16), np.ascontiguousarray(accept, np.int16),
+                      np.ascontiguousarray(lhs, np.int32), np.ascontiguousarray(rhs_offsets, np.int32),
+                      np.ascontiguousarray(rhs if len(rhs) else np.zeros(1), np.int32),
+                      np.ascontiguousarray(vocab_bytes if len(vocab_bytes) else np.zeros(1), np.uint8),
+                      np.ascontiguousarray(vocab_offsets, np.int32)]
+        tr, ac, lh, ro, rh, vb, vo = self._keep
+        self.num_states = int(tr.shape[0])
+        self.vocab_size = int(vo.shape[0] - 1)
+        lx = _Lexer(self.num_states, tr.ctypes.data, ac.ctypes.data)
+        gr = _Grammar(num_terminals, num_nonterminals, start, int(lh.shape[0]), lh.ctypes.data, ro.ctypes.data,
+                      rh.ctypes.data)
+        vc = _Vocab(self.vocab_size, vb.ctypes.data, vo.ctypes.data)
+        h = ctypes.c_void_p()
+        _check("epic_ctx_create", lib().epic_ctx_create(ctypes.byref(lx), ctypes.byref(gr), ctypes.byref(vc),
+                                                         max_batch, max_seq_len, max_cands, ctypes.byref(h)))
+        self._h = h
+
+    @classmethod
+    def from_problem(cls, p, max_batch, max_seq_len, max_cands):
+        """From an object with the generator's arrays (trans, accept, T, N, start, lhs, roff, rhs, vbytes, voffs)."""
+        return cls(p.trans, p.accept, p.T, p.N, p.start, p.lhs, p.roff, p.rhs, p.vbytes, p.voffs,
+                   max_batch, max_seq_len, max_cands)
+
+    def close(self):
+        if getattr(self, "_h", None):
+            lib().epic_ctx_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    @property
+    def workspace_bytes(self) -> int:
+        return int(lib().epic_workspace_bytes(self._h))
+
+    @property
+    def gap_classes(self) -> int:
+        return int(lib().epic_gap_classes(self._h))
+
+    def alloc_workspace(self, device="cuda"):
+        import torch
+
+        return torch.empty(self.workspace_bytes + 256, dtype=torch.uint8, device=device)
+
+    def lexmemo_build(self, stream=None):
+        _check("epic_lexmemo_build", lib().epic_lexmemo_build(self._h, _stream(stream)))
+
+    def memo_export(self) -> np.ndarray:
+        out = np.zeros((self.vocab_size, self.num_states, 16), dtype=np.uint8)
+        _check("epic_memo_export", lib().epic_memo_export(self._h, out.ctypes.data, out.nbytes))
+        return out
+
+    @staticmethod
+    def _ws(workspace):
+        p = _ptr(workspace)
+        aligned = (p + 255) & ~255
+        return aligned, workspace.numel() - (aligned - p)
+
+    def validate(self, seqs, cand_seq, cand_pos, cand_tok, verdict, workspace, stream=None):
+        B, n = (int(seqs.shape[0]), int(seqs.shape[1])) if seqs.dim() == 2 else (0, 0)
+        wp, wb = self._ws(workspace)
+        _check("epic_validate_batch", lib().epic_validate_batch(
+            self._h, _ptr(seqs), B, n, _ptr(cand_seq), _ptr(cand_pos), _ptr(cand_tok), int(cand_seq.numel()),
+            _ptr(verdict), wp, wb, _stream(stream)))
+
+    def select(self, seqs, cand_seq, cand_pos, cand_tok, conf, verdict, selected, workspace, counts=None,
+               stream=None):
+        B, n = int(seqs.shape[0]), int(seqs.shape[1])
+        wp, wb = self._ws(workspace)
+        _check("epic_select_compatible", lib().epic_select_compatible(
+            self._h, _ptr(seqs), B, n, _ptr(cand_seq), _ptr(cand_pos), _ptr(cand_tok), _ptr(conf), _ptr(verdict),
+            int(cand_seq.numel()), _ptr(selected), _ptr(counts), wp, wb, _stream(stream)))
+
+    def device_error(self, stream=None) -> int:
+        f = ctypes.c_uint32(0)
+        _check("epic_ctx_device_error", lib().epic_ctx_device_error(self._h, _stream(stream), ctypes.byref(f)))
+        return int(f.value)

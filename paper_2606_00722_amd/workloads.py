@@ -307,3 +307,26 @@ def run_steps(inst: Instance, validate: Callable, select: Callable, steps: Optio
         c = commit(inst, props, v, s)
         out.append(StepRecord(x, props, v, s, c))
     return out
+
+
+@dataclass
+class Arrays:
+    """Lexer DFA, grammar and vocabulary as the plain arrays both sides consume."""
+
+    trans: np.ndarray
+    accept: np.ndarray
+    T: int
+    N: int
+    start: int
+    lhs: np.ndarray
+    roff: np.ndarray
+    rhs: np.ndarray
+    vbytes: np.ndarray
+    voffs: np.ndarray
+
+
+def arrays(lang: G.Language, vocab: Vocab) -> Arrays:
+    tb = lang.tables
+    T, N, start, lhs, roff, rhs = lang.grammar.arrays()
+    vb, vo = vocab.csr()
+    return Arrays(tb.trans, tb.accept, T, N, start, lhs, roff, rhs, vb, vo)

@@ -1,0 +1,210 @@
+"""Bit-exact parity of the HIP path (through the C ABI) with the CPU oracle."""
+import os
+
+import numpy as np
+import pytest
+
+from paper_2606_00722_amd import grammars as G
+from paper_2606_00722_amd import workloads as W
+from tests.util import custom_vocab
+
+pytestmark = pytest.mark.gpu
+NTH = min(16, os.cpu_count() or 1)
+
+
+@pytest.fixture(scope="module")
+def gpu_mod():
+    import torch
+
+    if not torch.cuda.is_available():
+        pytest.fail("no GPU visible to the gpu-marked tests")
+    from tests import gpu_util
+
+    return gpu_util
+
+
+_cache = {}
+
+
+def setup(preset, gpu_mod, oracle_lib, seed=42):
+    key = (preset, seed)
+    if key not in _cache:
+        inst = W.make_instance(preset, seed)
+        arr = W.arrays(inst.lang, inst.vocab)
+        props = inst.cfg["props"] * inst.B
+        g = gpu_mod.Gpu(arr, inst.B, inst.n, max(props, 64))
+        _cache[key] = (inst, g, oracle_lib.problem_from(inst.lang, inst.vocab))
+    return _cache[key]
+
+
+@pytest.mark.parametrize("preset", [1, 2, 3, 4, 5])
+def test_memo_table_bit_exact(preset, gpu_mod, oracle_lib):
+    inst, g, p = setup(preset, gpu_mod, oracle_lib)
+    got = g.ctx.memo_export()
+    want = oracle_lib.memo(p)
+    assert got.shape == want.shape
+    assert np.array_equal(got, want)
+
+
+@pytest.mark.parametrize("preset", [1, 2])
+def test_verdicts_all_candidates(preset, gpu_mod, oracle_lib):
+    inst = W.make_instance(preset, 42)
+    _, g, p = setup(preset, gpu_mod, oracle_lib)
+    pr = W.propose(inst)
+    got = g.validate(inst.seqs, pr.seq, pr.pos, pr.tok)
+    want = oracle_lib.validate_batch(p, inst.seqs, pr.seq, pr.pos, pr.tok, NTH)
+    assert g.errors() == 0
+    assert np.array_equal(got, want)
+    assert 0 < int(want.sum()) < len(want)
+
+
+@pytest.mark.parametrize("preset,sample", [(3, 24), (4, 8), (5, 32)])
+def test_verdicts_full_batch_sampled(preset, sample, gpu_mod, oracle_lib):
+    """The whole step-1 batch on the GPU (the launch the benchmark times);
+    the oracle decides a seeded sample of the candidates one by one."""
+    inst = W.make_instance(preset, 42)
+    _, g, p = setup(preset, gpu_mod, oracle_lib)
+    pr = W.propose(inst)
+    got = g.validate(inst.seqs, pr.seq, pr.pos, pr.tok)
+    assert g.errors() == 0
+    assert set(np.unique(got).tolist()) <= {0, 1}
+    idx = np.random.default_rng(preset).choice(pr.C, min(sample, pr.C), replace=False)
+    want = oracle_lib.validate_batch(p, inst.seqs, pr.seq[idx], pr.pos[idx], pr.tok[idx], NTH)
+    assert np.array_equal(got[idx], want)
+
+
+@pytest.mark.parametrize("preset", [1, 2])
+def test_selection_matches_alg4(preset, gpu_mod, oracle_lib):
+    inst = W.make_instance(preset, 42)
+    _, g, p = setup(preset, gpu_mod, oracle_lib)
+    pr = W.propose(inst)
+    v = oracle_lib.validate_batch(p, inst.seqs, pr.seq, pr.pos, pr.tok, NTH)
+    got, counts = g.select(inst.seqs, pr.seq, pr.pos, pr.tok, pr.conf, v)
+    want, ocounts, status = oracle_lib.select(p, inst.seqs, pr.seq, pr.pos, pr.tok, pr.conf, v, NTH)
+    assert status == 0 and g.errors() == 0
+    assert np.array_equal(got, want)
+    assert counts == ocounts
+
+
+@pytest.mark.parametrize("preset,nseq", [(3, 3), (5, 6)])
+def test_selection_sampled_sequences(preset, nseq, gpu_mod, oracle_lib):
+    inst = W.make_instance(preset, 42)
+    _, g, p = setup(preset, gpu_mod, oracle_lib)
+    pr = W.propose(inst)
+    v = g.validate(inst.seqs, pr.seq, pr.pos, pr.tok)
+    got, _ = g.select(inst.seqs, pr.seq, pr.pos, pr.tok, pr.conf, v)
+    assert g.errors() == 0
+    seqs = np.random.default_rng(preset).choice(inst.B, nseq, replace=False)
+    idx = np.flatnonzero(np.isin(pr.seq, seqs))
+    want, _, status = oracle_lib.select(p, inst.seqs, pr.seq[idx], pr.pos[idx], pr.tok[idx], pr.conf[idx], v[idx], NTH)
+    assert status == 0
+    assert np.array_equal(got[idx], want)
+
+
+@pytest.mark.parametrize("preset", [1, 2])
+def test_multistep_evolution(preset, gpu_mod, oracle_lib):
+    """Every step: verdicts, selections and the committed sequences agree."""
+    _, g, p = setup(preset, gpu_mod, oracle_lib)
+    a, b = W.make_instance(preset, 43), W.make_instance(preset, 43)
+    ra = W.run_steps(a, lambda x, pr: g.validate(x, pr.seq, pr.pos, pr.tok),
+                     lambda x, pr, v: g.select(x, pr.seq, pr.pos, pr.tok, pr.conf, v)[0])
+    rb = W.run_steps(b, lambda x, pr: oracle_lib.validate_batch(p, x, pr.seq, pr.pos, pr.tok, NTH),
+                     lambda x, pr, v: oracle_lib.select(p, x, pr.seq, pr.pos, pr.tok, pr.conf, v, NTH)[0])
+    for sa, sb in zip(ra, rb):
+        assert np.array_equal(sa.seqs, sb.seqs)
+        assert np.array_equal(sa.verdict, sb.verdict)
+        assert np.array_equal(sa.selected, sb.selected)
+    assert np.array_equal(a.seqs, b.seqs)
+
+
+@pytest.mark.parametrize("name,extra", [("tiny_paren", ["((", "))", "()"]), ("tiny_expr", ["a+", "(a", "a)", " a"]),
+                                        ("tiny_kw", ["if", "(x", "x)", " i"]), ("tiny_ab", ["ab", "ba", "cc"]),
+                                        ("arith", ["a+", "1*", "(a", " 1"])])
+def test_tiny_languages(name, extra, gpu_mod, oracle_lib):
+    """Small random sequences: nullable start, multi-class gaps (no
+    whitespace), keyword/identifier boundaries spanning masks."""
+    lang = G.language(name)
+    vocab = custom_vocab(lang, extra)
+    arr = W.arrays(lang, vocab)
+    p = oracle_lib.problem_from(lang, vocab)
+    g = gpu_mod.Gpu(arr, 64, 10, 512)
+    rng = np.random.default_rng(4)
+    B, n = 48, 10
+    seqs = rng.integers(0, vocab.size, size=(B, n)).astype(np.int32)
+    seqs[rng.random((B, n)) < 0.5] = -1
+    for b in range(B):
+        seqs[b, rng.integers(0, n)] = -1
+    cs, cp, ct, cf = [], [], [], []
+    for b in range(B):
+        m = np.flatnonzero(seqs[b] == -1)
+        for pos in rng.choice(m, min(len(m), 4), replace=False):
+            cs.append(b), cp.append(pos), ct.append(rng.integers(0, vocab.size)), cf.append(rng.random())
+    cs, cp, ct = (np.array(a, np.int32) for a in (cs, cp, ct))
+    cf = np.array(cf, np.float32)
+    got = g.validate(seqs, cs, cp, ct)
+    want = oracle_lib.validate_batch(p, seqs, cs, cp, ct)
+    assert np.array_equal(got, want)
+    gs, gc = g.select(seqs, cs, cp, ct, cf, want)
+    ws, wc, st = oracle_lib.select(p, seqs, cs, cp, ct, cf, want)
+    assert st == 0 and g.errors() == 0
+    assert np.array_equal(gs, ws) and gc == wc
+
+
+def test_edge_cases(gpu_mod, oracle_lib):
+    """Single-token sequences, all-masked rows, candidates at both ends, the
+    longest row (every token of a 10-token row fixed but one), and C = 0."""
+    lang = G.language("arith")
+    vocab = custom_vocab(lang, ["a+", " 1", "((", "))"])
+    arr = W.arrays(lang, vocab)
+    p = oracle_lib.problem_from(lang, vocab)
+    g = gpu_mod.Gpu(arr, 8, 10, 64)
+    idx = {s: i for i, s in enumerate(vocab.strings)}
+    rows = [[-1] * 10, [-1] + [idx[b"a"]] * 9, [idx[b"("]] * 9 + [-1], [-1, idx[b"a+"], -1, -1, idx[b"))"], -1, -1, -1, -1, -1]]
+    seqs = np.array(rows, np.int32)
+    cs = np.array([0, 0, 1, 2, 3, 3], np.int32)
+    cp = np.array([0, 9, 0, 9, 0, 9], np.int32)
+    ct = np.array([idx[b"a"], idx[b")"], idx[b"("], idx[b")"], idx[b"(("], idx[b"1"]], np.int32)
+    got = g.validate(seqs, cs, cp, ct)
+    want = oracle_lib.validate_batch(p, seqs, cs, cp, ct)
+    assert np.array_equal(got, want)
+    one = np.array([[-1]], np.int32)
+    for t in range(vocab.size):
+        assert g.validate(one, [0], [0], [t])[0] == oracle_lib.validate_batch(p, one, [0], [0], [t])[0]
+    assert g.validate(seqs, np.zeros(0, np.int32), np.zeros(0, np.int32), np.zeros(0, np.int32)).size == 0
+
+
+def test_malformed_candidates_and_host_errors(gpu_mod, oracle_lib):
+    from paper_2606_00722_amd import epic
+
+    inst, g, p = setup(1, gpu_mod, oracle_lib)
+    x = inst.seqs
+    fixed = int(np.flatnonzero(x[0] != -1)[0])
+    masked = int(np.flatnonzero(x[0] == -1)[0])
+    seq = [0, 0, 5, 0, 0, -1]
+    pos = [fixed, masked, masked, 999, masked, masked]
+    tok = [1, inst.vocab.size, 1, 1, 3, 3]
+    got = g.validate(x, seq, pos, tok)
+    assert got.tolist()[:4] == [2, 2, 2, 2] and got[5] == 2
+    assert got[4] == oracle_lib.validate_batch(p, x, [0], [masked], [3])[0]
+    assert g.errors() & epic.DEV_BAD_CANDIDATE
+    assert g.errors() == 0  # reading clears
+    with pytest.raises(epic.EpicError) as e:  # more candidates than the context was sized for
+        n = 10_000
+        g.validate(x, np.zeros(n, np.int32), np.full(n, masked, np.int32), np.zeros(n, np.int32))
+    assert e.value.code == -3
+    # duplicate positions among valid candidates: nothing selected, flag set
+    v = np.array([1, 1], np.uint8)
+    sel, _ = g.select(x, [0, 0], [masked, masked], [3, 4], [0.5, 0.4], v)
+    assert sel.tolist() == [0, 0] and g.errors() & epic.DEV_BAD_SELECT
+
+
+def test_deterministic(gpu_mod, oracle_lib):
+    inst = W.make_instance(2, 42)
+    _, g, p = setup(2, gpu_mod, oracle_lib)
+    pr = W.propose(inst)
+    a = g.validate(inst.seqs, pr.seq, pr.pos, pr.tok)
+    b = g.validate(inst.seqs, pr.seq, pr.pos, pr.tok)
+    assert np.array_equal(a, b)
+    sa, _ = g.select(inst.seqs, pr.seq, pr.pos, pr.tok, pr.conf, a)
+    sb, _ = g.select(inst.seqs, pr.seq, pr.pos, pr.tok, pr.conf, a)
+    assert np.array_equal(sa, sb)
