@@ -52,6 +52,9 @@ typedef enum {
 #define EPIC_DEV_BAD_CANDIDATE 1u  /* position not masked, token/sequence/position out of range */
 #define EPIC_DEV_CAPACITY 2u       /* a chart or graph buffer overflowed: verdict 2 written */
 #define EPIC_DEV_BAD_SELECT 4u     /* duplicate positions or NaN confidence among valid candidates */
+/* With EPIC_DEV_CAPACITY, bit 8+i names the buffer that overflowed: i = 1 chart
+ * slots of one row, 2 slot hash, 3 row tasks, 4 chart entries, 5 graph nodes,
+ * 6 in-edges of a node, 7 frontier, 8 emission events. */
 
 typedef struct epic_ctx epic_ctx;
 
@@ -72,7 +75,8 @@ typedef struct {
 /* Grammar G = (V, Sigma_lex, P, S) (Sec. 3).  Terminals are 0..T-1,
  * nonterminals T..T+N-1; production p is lhs[p] -> rhs[rhs_offsets[p] ..
  * rhs_offsets[p+1]).  Empty right-hand sides are allowed.
- * Supported: T <= 63, N <= 64, at most 1024 dotted items (sum of |rhs|+1). */
+ * Supported: T <= 63, N <= 64, at most 512 dotted items (sum of |rhs|+1,
+ * plus two for the augmented start production). */
 typedef struct {
   int32_t num_terminals, num_nonterminals, start, num_productions;
   const int32_t* lhs;
@@ -92,7 +96,8 @@ typedef struct {
  * (dotted items, prediction closure, the lexer's gap automaton reduced to its
  * left-language classes, the regular cover of App. A.2), uploads them and
  * allocates the memo table (vocab_size * num_states * 16 bytes).  max_batch,
- * max_seq_len and max_cands bound later calls.  *out receives the context. */
+ * max_seq_len and max_cands bound later calls (max_seq_len <= 1024).
+ * *out receives the context. */
 epic_status epic_ctx_create(const epic_lexer_desc* lexer, const epic_grammar_desc* grammar,
                             const epic_vocab_desc* vocab, int32_t max_batch, int32_t max_seq_len,
                             int32_t max_cands, epic_ctx** out);
@@ -103,8 +108,10 @@ void epic_ctx_destroy(epic_ctx* ctx);
  * epic_select_compatible need (the caller allocates it, 256-byte aligned). */
 size_t epic_workspace_bytes(const epic_ctx* ctx);
 
-/* Number of gap classes of the lexer (diagnostics; 1 for lexers whose
- * whitespace can separate any two lexemes). */
+/* Number of graph nodes one masked run contributes: the left-language
+ * classes of the lexer's gap automaton (diagnostics; 2 for lexers whose
+ * whitespace can separate any two lexemes: inside whitespace, and after
+ * anything else). */
 int32_t epic_gap_classes(const epic_ctx* ctx);
 
 /* Alg. 2, lexing memoization: for every token t and lexer state q the greedy
@@ -144,7 +151,10 @@ epic_status epic_validate_batch(epic_ctx* ctx, const int32_t* d_seqs, int32_t B,
  * the exact check is Valid.  d_selected: uint8 [C], 1 = in the returned
  * subset B (empty, or at least two candidates whose joint application is
  * exactly valid).  A sequence whose verdict-1 candidates repeat a position or
- * carry a NaN confidence selects nothing and sets EPIC_DEV_BAD_SELECT.
+ * carry a NaN confidence selects nothing and sets EPIC_DEV_BAD_SELECT; one
+ * with more than 64 verdict-1 candidates selects nothing and sets
+ * EPIC_DEV_CAPACITY; a verdict-1 candidate that is not a legal update sets
+ * EPIC_DEV_BAD_CANDIDATE.
  * d_counts (optional, device int64 [2]) accumulates the number of cover and
  * exact checks performed. */
 epic_status epic_select_compatible(epic_ctx* ctx, const int32_t* d_seqs, int32_t B, int32_t n,
@@ -157,6 +167,14 @@ epic_status epic_select_compatible(epic_ctx* ctx, const int32_t* d_seqs, int32_t
 /* Synchronise `stream`, then read and clear the sticky device error bits
  * (EPIC_DEV_*) into *flags. */
 epic_status epic_ctx_device_error(epic_ctx* ctx, hipStream_t stream, uint32_t* flags);
+
+/* Diagnostics: synchronise `stream`, then read and clear the work counters
+ * accumulated by all walks since the last call: out[0] graph walks (one per
+ * validity or cover check), out[1] chart entries written (origin slots of
+ * Earley rows; 4*W + 2 bytes each for W item words), out[2] memo entries read
+ * (16 bytes each), out[3] graph nodes built, out[4] chart entries examined by
+ * completion and scan steps, out[5] of those, entries whose items were read. */
+epic_status epic_ctx_work_counters(epic_ctx* ctx, hipStream_t stream, int64_t* out);
 
 const char* epic_status_string(epic_status s);
 

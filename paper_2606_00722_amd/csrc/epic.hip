@@ -27,6 +27,7 @@
 namespace epic {
 
 #define EPIC_DEV __device__ inline
+#define EPIC_NOINLINE
 
 __device__ inline int tid() { return (int)threadIdx.x; }
 __device__ inline int nthreads() { return (int)blockDim.x; }
@@ -36,16 +37,33 @@ __device__ inline uint64_t at_or64(uint64_t* p, uint64_t v) {
   return (uint64_t)atomicOr((unsigned long long*)p, (unsigned long long)v);
 }
 __device__ inline int at_add32(int32_t* p, int v) { return atomicAdd(p, v); }
+__device__ inline unsigned long long at_add64(unsigned long long* p, unsigned long long v) { return atomicAdd(p, v); }
 __device__ inline uint32_t at_cas32(uint32_t* p, uint32_t cmp, uint32_t val) { return atomicCAS(p, cmp, val); }
 __device__ inline int at_min32(int32_t* p, int v) { return atomicMin(p, v); }
+// lane groups: G consecutive lanes of a wavefront (G a power of two <= 64)
+__device__ inline uint32_t grp_shfl(uint32_t v, int src, int G) { return (uint32_t)__shfl((int)v, src, G); }
+__device__ inline uint32_t grp_shfl_up1(uint32_t v, int G) { return (uint32_t)__shfl_up((int)v, 1u, G); }
+__device__ inline uint32_t grp_or32(uint32_t v, int G) {
+  for (int d = 1; d < G; d <<= 1) v |= (uint32_t)__shfl_xor((int)v, d, G);
+  return v;
+}
+__device__ inline uint64_t grp_or64(uint64_t v, int G) {
+  uint32_t lo = grp_or32((uint32_t)v, G), hi = grp_or32((uint32_t)(v >> 32), G);
+  return ((uint64_t)hi << 32) | lo;
+}
+__device__ inline uint64_t grp_bcast64(uint64_t v, int G) {
+  uint32_t lo = grp_shfl((uint32_t)v, 0, G), hi = grp_shfl((uint32_t)(v >> 32), 0, G);
+  return ((uint64_t)hi << 32) | lo;
+}
 
 #include "walker.inc"
 
-constexpr int kThreads = 256;
+constexpr int kThreads = 256;     // four wavefronts per walk
+constexpr int kMemoThreads = 256;
 
 // ------------------------------------------------------------------ memo
-__global__ void __launch_bounds__(kThreads) lexmemo_kernel(DevTab tb, uint4* memo) {
-  const size_t i = (size_t)blockIdx.x * kThreads + threadIdx.x;
+__global__ void __launch_bounds__(kMemoThreads) lexmemo_kernel(DevTab tb, uint4* memo) {
+  const size_t i = (size_t)blockIdx.x * kMemoThreads + threadIdx.x;
   if (i >= (size_t)tb.V * tb.Q) return;
   const int t = (int)(i / tb.Q), q0 = (int)(i % tb.Q);
   const int beg = tb.voffs[t], len = tb.voffs[t + 1] - beg;
@@ -86,7 +104,7 @@ __global__ void __launch_bounds__(kThreads) lexmemo_kernel(DevTab tb, uint4* mem
 struct WsArgs {
   char* base;
   size_t slot_bytes;
-  size_t off_cnt, off_org, off_sum, off_bits, off_cov, off_tqn, off_tqm;
+  size_t off_cnt, off_org, off_sum, off_bits, off_cov, off_tqn, off_tqm, off_tqM;
   int maxn, maxe, tcap;
 };
 
@@ -101,6 +119,7 @@ __device__ inline WgWork slot_work(const WsArgs& a, int slot) {
   w.cov = (uint32_t*)(b + a.off_cov);
   w.tq_node = (uint32_t*)(b + a.off_tqn);
   w.tq_mask = (uint64_t*)(b + a.off_tqm);
+  w.tq_M = (uint32_t*)(b + a.off_tqM);
   w.maxn = a.maxn;
   w.maxe = a.maxe;
   w.tcap = a.tcap;
@@ -116,6 +135,7 @@ __global__ void __launch_bounds__(kThreads) validate_kernel(DevTab tb, const int
                                                             uint8_t* __restrict__ verdict, WsArgs ws) {
   __shared__ Lds<W> L;
   const WgWork wk = slot_work(ws, blockIdx.x);
+  stage_tables<W>(tb, L);
   for (int c = blockIdx.x; c < C; c += gridDim.x) {
     const int b = cseq[c], i = cpos[c], t = ctok[c];
     const bool bad = b < 0 || b >= B || i < 0 || i >= n || t < 0 || t >= tb.V || seqs[(size_t)b * n + i] >= 0;
@@ -142,10 +162,10 @@ __global__ void __launch_bounds__(kThreads) validate_kernel(DevTab tb, const int
       __syncthreads();
       continue;
     }
-    const int r = walk<W, false>(tb, L, wk, n);
+    const int r = walk<W, W, false>(tb, L, wk, n);
     if (threadIdx.x == 0) {
       verdict[c] = (uint8_t)(r < 0 ? 2 : r);
-      if (r < 0) atomicOr(tb.dev_err, (uint32_t)EPIC_DEV_CAPACITY);
+      if (r < 0) atomicOr(tb.dev_err, (uint32_t)EPIC_DEV_CAPACITY | (1u << (8 + (L.overflow & 15))));
     }
     __syncthreads();
   }
@@ -190,6 +210,7 @@ __global__ void __launch_bounds__(kThreads) select_kernel(DevTab tb, const int32
   const int b = blockIdx.x;
   if (b >= B) return;
   const WgWork wk = slot_work(ws, blockIdx.x);
+  stage_tables<W>(tb, L);
   if (threadIdx.x == 0) {
     L.sel_n = 0;
     L.sel_bad = 0;
@@ -350,10 +371,10 @@ __global__ void __launch_bounds__(kThreads) select_kernel(DevTab tb, const int32
     __syncthreads();
     int r;
     if (req == kReqCover) {
-      r = walk<W, true>(tb, L, wk, n);
+      r = walk<W, W, true>(tb, L, wk, n);
       ++ncover;
     } else {
-      r = walk<W, false>(tb, L, wk, n);
+      r = walk<W, W, false>(tb, L, wk, n);
       ++nexact;
     }
     if (r < 0) {
@@ -369,7 +390,7 @@ __global__ void __launch_bounds__(kThreads) select_kernel(DevTab tb, const int32
       atomicAdd((unsigned long long*)&counts[1], (unsigned long long)nexact);
     }
     if (failed) {
-      atomicOr(tb.dev_err, (uint32_t)EPIC_DEV_CAPACITY);
+      atomicOr(tb.dev_err, (uint32_t)EPIC_DEV_CAPACITY | (1u << (8 + (L.overflow & 15))));
     } else {
       for (int i = 0; i < L.sel_n; ++i)
         if ((final_B >> i) & 1) selected[L.sel_idx[i]] = 1;
@@ -387,7 +408,7 @@ struct epic_ctx {
   int max_batch = 0, max_seq = 0, max_cands = 0;
   int maxn = 0, maxe = 0, nslot = 0;
   size_t slot_bytes = 0, ws_bytes = 0;
-  size_t off_cnt = 0, off_org = 0, off_sum = 0, off_bits = 0, off_cov = 0, off_tqn = 0, off_tqm = 0;
+  size_t off_cnt = 0, off_org = 0, off_sum = 0, off_bits = 0, off_cov = 0, off_tqn = 0, off_tqm = 0, off_tqM = 0;
   int tcap = 0;
   void* d_tables = nullptr;
   uint4* d_memo = nullptr;
@@ -456,6 +477,7 @@ epic_status upload(epic_ctx* c) {
   t.voffs = (const int32_t*)(d + o_vo);
   t.memo = c->d_memo;
   t.dev_err = c->d_err;
+  t.work = (unsigned long long*)((char*)c->d_err + 64);
   return EPIC_OK;
 }
 
@@ -470,6 +492,7 @@ WsArgs ws_args(const epic_ctx* c, void* ws) {
   a.off_cov = c->off_cov;
   a.off_tqn = c->off_tqn;
   a.off_tqm = c->off_tqm;
+  a.off_tqM = c->off_tqM;
   a.maxn = c->maxn;
   a.maxe = c->maxe;
   a.tcap = c->tcap;
@@ -514,6 +537,15 @@ struct SelectLaunch {
 
 extern "C" {
 
+epic_status epic_ctx_work_counters(epic_ctx* c, hipStream_t stream, int64_t* out) {
+  if (!c || !out) return EPIC_ERR_NULL;
+  if (hipStreamSynchronize(stream) != hipSuccess) return EPIC_ERR_HIP;
+  if (hipMemcpy(out, (char*)c->d_err + 64, 6 * sizeof(int64_t), hipMemcpyDeviceToHost) != hipSuccess)
+    return EPIC_ERR_HIP;
+  if (hipMemset((char*)c->d_err + 64, 0, 6 * sizeof(int64_t)) != hipSuccess) return EPIC_ERR_HIP;
+  return EPIC_OK;
+}
+
 const char* epic_status_string(epic_status s) {
   switch (s) {
     case EPIC_OK: return "ok";
@@ -557,7 +589,7 @@ epic_status epic_ctx_create(const epic_lexer_desc* lexer, const epic_grammar_des
   const HostTables& H = c->H;
   // graph nodes: start, final, one per fixed byte, K per masked run
   c->maxn = 8 * max_seq_len + H.K * (max_seq_len / 2 + 2) + 4;
-  c->maxe = std::max(16384, 256 * max_seq_len);
+  c->maxe = std::min(std::max(16384, 512 * max_seq_len), 131072);
   c->tcap = 16384;
   c->nslot = std::min(std::max(max_cands, max_batch), 1024);
   c->off_cnt = align256((size_t)c->maxn * 4);
@@ -567,7 +599,8 @@ epic_status epic_ctx_create(const epic_lexer_desc* lexer, const epic_grammar_des
   c->off_cov = c->off_bits + align256((size_t)c->maxe * H.W * 4);
   c->off_tqn = c->off_cov + align256((size_t)c->maxn * H.CW * 4);
   c->off_tqm = c->off_tqn + align256((size_t)2 * c->tcap * 4);
-  c->slot_bytes = c->off_tqm + align256((size_t)2 * c->tcap * 8);
+  c->off_tqM = c->off_tqm + align256((size_t)2 * c->tcap * 8);
+  c->slot_bytes = c->off_tqM + align256((size_t)kTaskChunk * H.W * 4);
   c->ws_bytes = c->slot_bytes * c->nslot;
   epic_status s = upload(c);
   if (s != EPIC_OK) {
@@ -593,8 +626,8 @@ int32_t epic_gap_classes(const epic_ctx* c) { return c ? c->H.K : -1; }
 epic_status epic_lexmemo_build(epic_ctx* c, hipStream_t stream) {
   if (!c) return EPIC_ERR_NULL;
   const size_t total = (size_t)c->H.V * c->H.Q;
-  const unsigned grid = (unsigned)((total + kThreads - 1) / kThreads);
-  hipLaunchKernelGGL(lexmemo_kernel, dim3(grid), dim3(kThreads), 0, stream, c->tab, c->d_memo);
+  const unsigned grid = (unsigned)((total + kMemoThreads - 1) / kMemoThreads);
+  hipLaunchKernelGGL(lexmemo_kernel, dim3(grid), dim3(kMemoThreads), 0, stream, c->tab, c->d_memo);
   if (hipGetLastError() != hipSuccess) return EPIC_ERR_HIP;
   c->memo_built = true;
   return EPIC_OK;

@@ -23,7 +23,7 @@ DEV_BAD_CANDIDATE, DEV_CAPACITY, DEV_BAD_SELECT = 1, 2, 4
 
 FUNCTIONS = ["epic_ctx_create", "epic_ctx_destroy", "epic_workspace_bytes", "epic_gap_classes",
              "epic_lexmemo_build", "epic_memo_export", "epic_validate_batch", "epic_select_compatible",
-             "epic_ctx_device_error", "epic_status_string"]
+             "epic_ctx_device_error", "epic_ctx_work_counters", "epic_status_string"]
 
 
 class EpicError(RuntimeError):
@@ -74,6 +74,8 @@ def lib() -> ctypes.CDLL:
         L.epic_select_compatible.restype = ctypes.c_int
         L.epic_ctx_device_error.argtypes = [P, P, ctypes.POINTER(ctypes.c_uint32)]
         L.epic_ctx_device_error.restype = ctypes.c_int
+        L.epic_ctx_work_counters.argtypes = [P, P, P]
+        L.epic_ctx_work_counters.restype = ctypes.c_int
         L.epic_status_string.argtypes = [ctypes.c_int]
         L.epic_status_string.restype = ctypes.c_char_p
         _lib = L
@@ -176,6 +178,17 @@ class Context:
         _check("epic_select_compatible", lib().epic_select_compatible(
             self._h, _ptr(seqs), B, n, _ptr(cand_seq), _ptr(cand_pos), _ptr(cand_tok), _ptr(conf), _ptr(verdict),
             int(cand_seq.numel()), _ptr(selected), _ptr(counts), wp, wb, _stream(stream)))
+
+    def work_counters(self, stream=None) -> np.ndarray:
+        """int64[6]: walks, chart entries written, memo entries read, graph nodes,
+        chart entries examined, chart entries used (read and cleared)."""
+        out = np.zeros(6, dtype=np.int64)
+        _check("epic_ctx_work_counters", lib().epic_ctx_work_counters(self._h, _stream(stream), out.ctypes.data))
+        return out
+
+    @property
+    def item_words(self) -> int:
+        return int(getattr(self, "_item_words", 0))
 
     def device_error(self, stream=None) -> int:
         f = ctypes.c_uint32(0)
