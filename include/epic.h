@@ -171,9 +171,11 @@ epic_status epic_ctx_device_error(epic_ctx* ctx, hipStream_t stream, uint32_t* f
 /* Diagnostics: synchronise `stream`, then read and clear the work counters
  * accumulated by all walks since the last call: out[0] graph walks (one per
  * validity or cover check), out[1] chart entries written (origin slots of
- * Earley rows; 4*W + 2 bytes each for W item words), out[2] memo entries read
- * (16 bytes each), out[3] graph nodes built, out[4] chart entries examined by
- * completion and scan steps, out[5] of those, entries whose items were read. */
+ * Earley rows: 4*W bytes of items for W item words, an 8-byte summary of the
+ * expected nonterminals and a 2-byte origin), out[2] memo entries read (16
+ * bytes each), out[3] graph nodes built, out[4] chart entries examined by
+ * completion and scan steps (summary and origin read), out[5] of those,
+ * entries whose items were read. */
 epic_status epic_ctx_work_counters(epic_ctx* ctx, hipStream_t stream, int64_t* out);
 
 const char* epic_status_string(epic_status s);

@@ -17,7 +17,7 @@
 //    of the gap automaton's determinisation, over all entry states, agrees).
 //    Merging nodes with equal left languages keeps the language of the
 //    completion automaton, so Valid is unchanged.  For lexers where whitespace
-//    can separate any two lexemes this leaves one class per gap.
+//    can separate any two lexemes this leaves two classes per gap.
 //  * The regular cover of App. A.2: its rule-position states are the dotted
 //    items; entry/exit states of each nonterminal are extra bits.
 #include "tables.h"
