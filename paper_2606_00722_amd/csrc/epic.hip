@@ -58,7 +58,10 @@ __device__ inline uint64_t grp_bcast64(uint64_t v, int G) {
 
 #include "walker.inc"
 
-constexpr int kThreads = 256;     // four wavefronts per walk
+#ifndef EPIC_THREADS
+#define EPIC_THREADS 1024
+#endif
+constexpr int kThreads = EPIC_THREADS;  // threads per walk (at most 1024)
 constexpr int kMemoThreads = 256;
 
 // ------------------------------------------------------------------ memo
@@ -104,7 +107,7 @@ __global__ void __launch_bounds__(kMemoThreads) lexmemo_kernel(DevTab tb, uint4*
 struct WsArgs {
   char* base;
   size_t slot_bytes;
-  size_t off_cnt, off_org, off_sum, off_bits, off_cov, off_tqn, off_tqm, off_tqM;
+  size_t off_cnt, off_org, off_sum, off_bits, off_cov, off_tqn, off_tqm, off_tqM, off_tqo;
   int maxn, maxe, tcap;
 };
 
@@ -120,6 +123,7 @@ __device__ inline WgWork slot_work(const WsArgs& a, int slot) {
   w.tq_node = (uint32_t*)(b + a.off_tqn);
   w.tq_mask = (uint64_t*)(b + a.off_tqm);
   w.tq_M = (uint32_t*)(b + a.off_tqM);
+  w.tq_off = (int32_t*)(b + a.off_tqo);
   w.maxn = a.maxn;
   w.maxe = a.maxe;
   w.tcap = a.tcap;
@@ -408,7 +412,7 @@ struct epic_ctx {
   int max_batch = 0, max_seq = 0, max_cands = 0;
   int maxn = 0, maxe = 0, nslot = 0;
   size_t slot_bytes = 0, ws_bytes = 0;
-  size_t off_cnt = 0, off_org = 0, off_sum = 0, off_bits = 0, off_cov = 0, off_tqn = 0, off_tqm = 0, off_tqM = 0;
+  size_t off_cnt = 0, off_org = 0, off_sum = 0, off_bits = 0, off_cov = 0, off_tqn = 0, off_tqm = 0, off_tqM = 0, off_tqo = 0;
   int tcap = 0;
   void* d_tables = nullptr;
   uint4* d_memo = nullptr;
@@ -493,6 +497,7 @@ WsArgs ws_args(const epic_ctx* c, void* ws) {
   a.off_tqn = c->off_tqn;
   a.off_tqm = c->off_tqm;
   a.off_tqM = c->off_tqM;
+  a.off_tqo = c->off_tqo;
   a.maxn = c->maxn;
   a.maxe = c->maxe;
   a.tcap = c->tcap;
@@ -600,7 +605,8 @@ epic_status epic_ctx_create(const epic_lexer_desc* lexer, const epic_grammar_des
   c->off_tqn = c->off_cov + align256((size_t)c->maxn * H.CW * 4);
   c->off_tqm = c->off_tqn + align256((size_t)2 * c->tcap * 4);
   c->off_tqM = c->off_tqm + align256((size_t)2 * c->tcap * 8);
-  c->slot_bytes = c->off_tqM + align256((size_t)kTaskChunk * H.W * 4);
+  c->off_tqo = c->off_tqM + align256((size_t)kTaskChunk * H.W * 4);
+  c->slot_bytes = c->off_tqo + align256((size_t)kTaskChunk * 4);
   c->ws_bytes = c->slot_bytes * c->nslot;
   epic_status s = upload(c);
   if (s != EPIC_OK) {
