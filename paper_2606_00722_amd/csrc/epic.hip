@@ -42,7 +42,6 @@ __device__ inline uint32_t at_cas32(uint32_t* p, uint32_t cmp, uint32_t val) { r
 __device__ inline int at_min32(int32_t* p, int v) { return atomicMin(p, v); }
 // lane groups: G consecutive lanes of a wavefront (G a power of two <= 64)
 __device__ inline uint32_t grp_shfl(uint32_t v, int src, int G) { return (uint32_t)__shfl((int)v, src, G); }
-__device__ inline uint32_t grp_shfl_up1(uint32_t v, int G) { return (uint32_t)__shfl_up((int)v, 1u, G); }
 __device__ inline uint32_t grp_or32(uint32_t v, int G) {
   for (int d = 1; d < G; d <<= 1) v |= (uint32_t)__shfl_xor((int)v, d, G);
   return v;
@@ -51,17 +50,13 @@ __device__ inline uint64_t grp_or64(uint64_t v, int G) {
   uint32_t lo = grp_or32((uint32_t)v, G), hi = grp_or32((uint32_t)(v >> 32), G);
   return ((uint64_t)hi << 32) | lo;
 }
-__device__ inline uint64_t grp_bcast64(uint64_t v, int G) {
-  uint32_t lo = grp_shfl((uint32_t)v, 0, G), hi = grp_shfl((uint32_t)(v >> 32), 0, G);
-  return ((uint64_t)hi << 32) | lo;
-}
 
 #include "walker.inc"
 
-#ifndef EPIC_THREADS
-#define EPIC_THREADS 1024
-#endif
-constexpr int kThreads = EPIC_THREADS;  // threads per walk (at most 1024)
+// Threads per walk: one lane group of W lanes per chart entry; wide item sets
+// (W = 16) get 32 groups, narrow ones 64 to 256.
+template <int W>
+constexpr int threads_for() { return W >= 16 ? 512 : 256; }
 constexpr int kMemoThreads = 256;
 
 // ------------------------------------------------------------------ memo
@@ -107,8 +102,8 @@ __global__ void __launch_bounds__(kMemoThreads) lexmemo_kernel(DevTab tb, uint4*
 struct WsArgs {
   char* base;
   size_t slot_bytes;
-  size_t off_cnt, off_org, off_sum, off_bits, off_cov, off_tqn, off_tqm, off_tqM, off_tqo;
-  int maxn, maxe, tcap;
+  size_t off_cnt, off_org, off_sn, off_st, off_bits, off_cov;
+  int maxn, maxe;
 };
 
 __device__ inline WgWork slot_work(const WsArgs& a, int slot) {
@@ -116,23 +111,19 @@ __device__ inline WgWork slot_work(const WsArgs& a, int slot) {
   WgWork w;
   w.row_off = (int32_t*)b;
   w.row_cnt = (int32_t*)(b + a.off_cnt);
-  w.ent_org = (uint16_t*)(b + a.off_org);
-  w.ent_sum = (uint64_t*)(b + a.off_sum);
+  w.ent_org = (int32_t*)(b + a.off_org);
+  w.ent_sn = (uint64_t*)(b + a.off_sn);
+  w.ent_st = (uint64_t*)(b + a.off_st);
   w.ent_bits = (uint32_t*)(b + a.off_bits);
   w.cov = (uint32_t*)(b + a.off_cov);
-  w.tq_node = (uint32_t*)(b + a.off_tqn);
-  w.tq_mask = (uint64_t*)(b + a.off_tqm);
-  w.tq_M = (uint32_t*)(b + a.off_tqM);
-  w.tq_off = (int32_t*)(b + a.off_tqo);
   w.maxn = a.maxn;
   w.maxe = a.maxe;
-  w.tcap = a.tcap;
   return w;
 }
 
 // ------------------------------------------------------------------ validate
 template <int W>
-__global__ void __launch_bounds__(kThreads) validate_kernel(DevTab tb, const int32_t* __restrict__ seqs, int B,
+__global__ void __launch_bounds__(threads_for<W>()) validate_kernel(DevTab tb, const int32_t* __restrict__ seqs, int B,
                                                             int n, const int32_t* __restrict__ cseq,
                                                             const int32_t* __restrict__ cpos,
                                                             const int32_t* __restrict__ ctok, int C,
@@ -152,7 +143,7 @@ __global__ void __launch_bounds__(kThreads) validate_kernel(DevTab tb, const int
     }
     if (threadIdx.x == 0) L.sel_bad = 0;
     __syncthreads();
-    for (int k = threadIdx.x; k < n; k += kThreads) {
+    for (int k = threadIdx.x; k < n; k += threads_for<W>()) {
       const int x = k == i ? t : seqs[(size_t)b * n + k];
       if (x < -1 || x >= tb.V) L.sel_bad = 1;
       L.xtok[k] = x;
@@ -199,7 +190,7 @@ __device__ inline void split_halves(uint64_t S, uint64_t& lo, uint64_t& hi) {
 }
 
 template <int W>
-__global__ void __launch_bounds__(kThreads) select_kernel(DevTab tb, const int32_t* __restrict__ seqs, int B, int n,
+__global__ void __launch_bounds__(threads_for<W>()) select_kernel(DevTab tb, const int32_t* __restrict__ seqs, int B, int n,
                                                           const int32_t* __restrict__ cseq,
                                                           const int32_t* __restrict__ cpos,
                                                           const int32_t* __restrict__ ctok,
@@ -220,7 +211,7 @@ __global__ void __launch_bounds__(kThreads) select_kernel(DevTab tb, const int32
     L.sel_bad = 0;
   }
   __syncthreads();
-  for (int c = threadIdx.x; c < C; c += kThreads) {
+  for (int c = threadIdx.x; c < C; c += threads_for<W>()) {
     if (cseq[c] != b) continue;
     selected[c] = 0;
     if (verdict[c] != 1) continue;
@@ -232,7 +223,7 @@ __global__ void __launch_bounds__(kThreads) select_kernel(DevTab tb, const int32
     int j = atomicAdd(&L.sel_n, 1);
     if (j < 64) L.sel_idx[j] = c;
   }
-  for (int k = threadIdx.x; k < n; k += kThreads) {
+  for (int k = threadIdx.x; k < n; k += threads_for<W>()) {
     const int x = seqs[(size_t)b * n + k];
     if (x < -1 || x >= tb.V) L.sel_bad = 3;
   }
@@ -366,7 +357,7 @@ __global__ void __launch_bounds__(kThreads) select_kernel(DevTab tb, const int32
     const int req = L.sel_req;
     if (req == kReqDone) break;
     const uint64_t msk = L.sel_mask;
-    for (int k = threadIdx.x; k < n; k += kThreads) L.xtok[k] = seqs[(size_t)b * n + k];
+    for (int k = threadIdx.x; k < n; k += threads_for<W>()) L.xtok[k] = seqs[(size_t)b * n + k];
     __syncthreads();
     if (threadIdx.x == 0) {
       for (int i = 0; i < L.sel_n; ++i)
@@ -412,8 +403,7 @@ struct epic_ctx {
   int max_batch = 0, max_seq = 0, max_cands = 0;
   int maxn = 0, maxe = 0, nslot = 0;
   size_t slot_bytes = 0, ws_bytes = 0;
-  size_t off_cnt = 0, off_org = 0, off_sum = 0, off_bits = 0, off_cov = 0, off_tqn = 0, off_tqm = 0, off_tqM = 0, off_tqo = 0;
-  int tcap = 0;
+  size_t off_cnt = 0, off_org = 0, off_sn = 0, off_st = 0, off_bits = 0, off_cov = 0;
   void* d_tables = nullptr;
   uint4* d_memo = nullptr;
   uint32_t* d_err = nullptr;
@@ -441,7 +431,8 @@ epic_status upload(epic_ctx* c) {
          o_flush = place(blob, H.flushlab), o_cexit = place(blob, H.cls_exit), o_cint = place(blob, H.cls_internal),
          o_centry = place(blob, H.cls_entry), o_cflush = place(blob, H.cls_flush), o_expt = place(blob, H.exp_t),
          o_expn = place(blob, H.exp_n), o_pred = place(blob, H.pred), o_comp = place(blob, H.complete),
-         o_lhs = place(blob, H.item_lhs), o_nnt = place(blob, H.next_nt), o_ccl = place(blob, H.cover_cl),
+         o_lhs = place(blob, H.item_lhs), o_nsym = place(blob, H.next_sym), o_mn = place(blob, H.mn),
+         o_gtm = place(blob, H.gap_tm), o_gown = place(blob, H.gap_own), o_ccl = place(blob, H.cover_cl),
          o_vb = place(blob, H.vbytes), o_vo = place(blob, H.voffs);
   if (hipMalloc(&c->d_tables, blob.size()) != hipSuccess) return EPIC_ERR_HIP;
   if (hipMemcpy(c->d_tables, blob.data(), blob.size(), hipMemcpyHostToDevice) != hipSuccess) return EPIC_ERR_HIP;
@@ -475,7 +466,11 @@ epic_status upload(epic_ctx* c) {
   t.pred = (const uint32_t*)(d + o_pred);
   t.complete = (const uint32_t*)(d + o_comp);
   t.item_lhs = (const int8_t*)(d + o_lhs);
-  t.next_nt = (const int8_t*)(d + o_nnt);
+  t.next_sym = (const int8_t*)(d + o_nsym);
+  t.mn = (const uint32_t*)(d + o_mn);
+  t.gap_tm = (const uint32_t*)(d + o_gtm);
+  t.gap_own = (const uint32_t*)(d + o_gown);
+  t.gap_eps = H.gap_eps;
   t.cover_cl = (const uint32_t*)(d + o_ccl);
   t.vbytes = (const uint8_t*)(d + o_vb);
   t.voffs = (const int32_t*)(d + o_vo);
@@ -491,16 +486,12 @@ WsArgs ws_args(const epic_ctx* c, void* ws) {
   a.slot_bytes = c->slot_bytes;
   a.off_cnt = c->off_cnt;
   a.off_org = c->off_org;
-  a.off_sum = c->off_sum;
+  a.off_sn = c->off_sn;
+  a.off_st = c->off_st;
   a.off_bits = c->off_bits;
   a.off_cov = c->off_cov;
-  a.off_tqn = c->off_tqn;
-  a.off_tqm = c->off_tqm;
-  a.off_tqM = c->off_tqM;
-  a.off_tqo = c->off_tqo;
   a.maxn = c->maxn;
   a.maxe = c->maxe;
-  a.tcap = c->tcap;
   return a;
 }
 
@@ -521,7 +512,7 @@ struct ValidateLaunch {
   static epic_status run(epic_ctx* c, const int32_t* seqs, int B, int n, const int32_t* cs, const int32_t* cp,
                          const int32_t* ct, int C, uint8_t* verdict, void* ws, hipStream_t stream) {
     int grid = std::min(C, c->nslot);
-    hipLaunchKernelGGL((validate_kernel<W>), dim3(grid), dim3(kThreads), 0, stream, c->tab, seqs, B, n, cs, cp, ct,
+    hipLaunchKernelGGL((validate_kernel<W>), dim3(grid), dim3(threads_for<W>()), 0, stream, c->tab, seqs, B, n, cs, cp, ct,
                        C, verdict, ws_args(c, ws));
     return hipGetLastError() == hipSuccess ? EPIC_OK : EPIC_ERR_HIP;
   }
@@ -532,7 +523,7 @@ struct SelectLaunch {
   static epic_status run(epic_ctx* c, const int32_t* seqs, int B, int n, const int32_t* cs, const int32_t* cp,
                          const int32_t* ct, const float* conf, const uint8_t* verdict, int C, uint8_t* sel,
                          int64_t* counts, void* ws, hipStream_t stream) {
-    hipLaunchKernelGGL((select_kernel<W>), dim3(B), dim3(kThreads), 0, stream, c->tab, seqs, B, n, cs, cp, ct, conf,
+    hipLaunchKernelGGL((select_kernel<W>), dim3(B), dim3(threads_for<W>()), 0, stream, c->tab, seqs, B, n, cs, cp, ct, conf,
                        verdict, C, sel, (long long*)counts, ws_args(c, ws));
     return hipGetLastError() == hipSuccess ? EPIC_OK : EPIC_ERR_HIP;
   }
@@ -595,18 +586,14 @@ epic_status epic_ctx_create(const epic_lexer_desc* lexer, const epic_grammar_des
   // graph nodes: start, final, one per fixed byte, K per masked run
   c->maxn = 8 * max_seq_len + H.K * (max_seq_len / 2 + 2) + 4;
   c->maxe = std::min(std::max(16384, 512 * max_seq_len), 131072);
-  c->tcap = 16384;
   c->nslot = std::min(std::max(max_cands, max_batch), 1024);
   c->off_cnt = align256((size_t)c->maxn * 4);
   c->off_org = c->off_cnt + align256((size_t)c->maxn * 4);
-  c->off_sum = c->off_org + align256((size_t)c->maxe * 2);
-  c->off_bits = c->off_sum + align256((size_t)c->maxe * 8);
+  c->off_sn = c->off_org + align256((size_t)c->maxe * 4);
+  c->off_st = c->off_sn + align256((size_t)c->maxe * 8);
+  c->off_bits = c->off_st + align256((size_t)c->maxe * 8);
   c->off_cov = c->off_bits + align256((size_t)c->maxe * H.W * 4);
-  c->off_tqn = c->off_cov + align256((size_t)c->maxn * H.CW * 4);
-  c->off_tqm = c->off_tqn + align256((size_t)2 * c->tcap * 4);
-  c->off_tqM = c->off_tqm + align256((size_t)2 * c->tcap * 8);
-  c->off_tqo = c->off_tqM + align256((size_t)kTaskChunk * H.W * 4);
-  c->slot_bytes = c->off_tqo + align256((size_t)kTaskChunk * 4);
+  c->slot_bytes = c->off_cov + align256((size_t)c->maxn * H.CW * 4);
   c->ws_bytes = c->slot_bytes * c->nslot;
   epic_status s = upload(c);
   if (s != EPIC_OK) {

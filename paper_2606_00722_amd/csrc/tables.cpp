@@ -142,25 +142,42 @@ int build_tables(int Q, const int16_t* trans, const int16_t* accept, int T, int 
   H.voffs.assign(voffs, voffs + V + 1);
 
   // ---------------------------------------------------------------- items
+  // Dotted items of production p are base[p] .. base[p]+|rhs_p|.  Productions
+  // are packed into 32-bit words first-fit by decreasing length, so that no
+  // production straddles a word: advancing the dot is then a shift inside
+  // one word, and closing an item set over a self-loop of the completion
+  // graph is one integer addition per word (the carry runs along a
+  // production's consecutive items and stops at its first item that cannot
+  // advance).
   std::vector<int> base(P + 1);
-  int ni = 0;
-  for (int p = 0; p < P; ++p) {
-    base[p] = ni;
-    int len = roff[p + 1] - roff[p];
-    ni += len + 1;
+  std::vector<int> order(P + 1);
+  for (int p = 0; p <= P; ++p) {
+    order[p] = p;
+    int len = p < P ? roff[p + 1] - roff[p] : 1;
     H.max_rhs = std::max(H.max_rhs, len);
+    if (len + 1 > 32) {
+      why = "a production has more than 31 symbols";
+      return EPIC_ERR_UNSUPPORTED;
+    }
   }
-  base[P] = ni;
-  ni += 2;  // S' -> . S and S' -> S .
-  H.max_rhs = std::max(H.max_rhs, 1);
-  H.NI = ni;
-  int words = (ni + 31) / 32;
+  auto plen = [&](int p) { return (p < P ? roff[p + 1] - roff[p] : 1) + 1; };
+  std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return plen(a) > plen(b); });
+  std::vector<int> fill;  // items used in each word
+  for (int p : order) {
+    int need = plen(p), w = 0;
+    while (w < (int)fill.size() && fill[w] + need > 32) ++w;
+    if (w == (int)fill.size()) fill.push_back(0);
+    base[p] = w * 32 + fill[w];
+    fill[w] += need;
+  }
   int W = 1;
-  while (W < words) W *= 2;
+  while (W < (int)fill.size()) W *= 2;
   if (W > kMaxItemWords) {
     why = "more than 512 dotted items";
     return EPIC_ERR_UNSUPPORTED;
   }
+  const int ni = W * 32;
+  H.NI = ni;
   H.W = W;
   H.CW = W + 4;  // cover state: items, then entry bits (2 words), then exit bits (2 words)
   H.start_nt = start - T;
@@ -172,6 +189,7 @@ int build_tables(int Q, const int16_t* trans, const int16_t* accept, int T, int 
   H.complete.assign(W, 0);
   H.item_lhs.assign(ni, -1);
   H.next_nt.assign(ni, -1);
+  H.next_sym.assign(ni, -1);
   H.start_of.assign((size_t)N * W, 0);
   H.end_of.assign((size_t)N * W, 0);
   for (int p = 0; p <= P; ++p) {
@@ -184,9 +202,11 @@ int build_tables(int Q, const int16_t* trans, const int16_t* accept, int T, int 
         int X = p < P ? rhs[roff[p] + k] : start;
         if (X < T) {
           set32(H.exp_t, (size_t)X * W, it);
+          H.next_sym[it] = (int8_t)X;
         } else {
           set32(H.exp_n, (size_t)(X - T) * W, it);
           H.next_nt[it] = (int8_t)(X - T);
+          H.next_sym[it] = (int8_t)(64 + X - T);
         }
       } else if (p < P) {
         set32(H.complete, 0, it);
@@ -197,24 +217,68 @@ int build_tables(int Q, const int16_t* trans, const int16_t* accept, int T, int 
       set32(H.end_of, (size_t)A * W, base[p] + len);
     }
   }
-  for (int B = 0; B < N; ++B) {  // left-corner closure
-    std::vector<char> in(N, 0);
-    in[B] = 1;
-    bool changed = true;
-    while (changed) {
-      changed = false;
-      for (int p = 0; p < P; ++p) {
-        int A = lhs[p] - T;
-        if (!in[A] || roff[p + 1] == roff[p]) continue;
-        int X = rhs[roff[p]];
-        if (X >= T && !in[X - T]) {
-          in[X - T] = 1;
-          changed = true;
-        }
+  // nullable nonterminals (derive the empty string)
+  uint64_t nullable = 0;
+  for (bool changed = true; changed;) {
+    changed = false;
+    for (int p = 0; p < P; ++p) {
+      int A = lhs[p] - T;
+      if ((nullable >> A) & 1) continue;
+      bool all = true;
+      for (int k = roff[p]; k < roff[p + 1] && all; ++k) all = rhs[k] >= T && ((nullable >> (rhs[k] - T)) & 1);
+      if (all) {
+        nullable |= 1ull << A;
+        changed = true;
       }
     }
-    for (int p = 0; p < P; ++p)
-      if (in[lhs[p] - T]) set32(H.pred, (size_t)B * W, base[p]);
+  }
+  H.nullable = nullable;
+  // item-set helpers over W words
+  typedef std::vector<uint32_t> Set;
+  auto exp_mask = [&](uint64_t nts) {
+    Set m(W, 0);
+    for (int B = 0; B < N; ++B)
+      if ((nts >> B) & 1)
+        for (int w = 0; w < W; ++w) m[w] |= H.exp_n[(size_t)B * W + w];
+    return m;
+  };
+  auto adv_or = [&](const Set& x, const Set& m, Set& out) {  // out |= (x & m) << 1, true if out grew
+    bool grew = false;
+    for (int w = 0; w < W; ++w) {
+      uint32_t a = (x[w] & m[w]) << 1;
+      if (a & ~out[w]) grew = true;
+      out[w] |= a;
+    }
+    return grew;
+  };
+  H.mn.assign(W, 0);
+  {
+    Set m = exp_mask(nullable);
+    for (int w = 0; w < W; ++w) H.mn[w] = m[w];
+  }
+  auto nclose = [&](Set& x) {  // advance over nullable nonterminals until nothing changes
+    while (adv_or(x, H.mn, x)) {
+    }
+  };
+  // Prediction closure of each nonterminal B: the items A -> . gamma for A
+  // predicted from B, closed under skipping nullable nonterminals and under
+  // predicting every nonterminal such an item expects (Alg. 3's predict step
+  // together with the empty completions of nullable nonterminals).
+  for (int B = 0; B < N; ++B) {
+    Set x(W, 0);
+    uint64_t predicted = 0, todo = 1ull << B;
+    while (todo) {
+      predicted |= todo;
+      for (int A = 0; A < N; ++A)
+        if ((todo >> A) & 1)
+          for (int w = 0; w < W; ++w) x[w] |= H.start_of[(size_t)A * W + w];
+      nclose(x);
+      uint64_t e = 0;
+      for (int i = 0; i < ni; ++i)
+        if (((x[i >> 5] >> (i & 31)) & 1) && H.next_nt[i] >= 0) e |= 1ull << H.next_nt[i];
+      todo = e & ~predicted;
+    }
+    for (int w = 0; w < W; ++w) H.pred[(size_t)B * W + w] = x[w];
   }
 
   // ---------------------------------------------------------------- cover
@@ -396,6 +460,102 @@ int build_tables(int Q, const int16_t* trans, const int16_t* accept, int T, int 
   for (int k = 0; k < K; ++k)
     for (int q = 0; q < Q; ++q)
       if ((H.cls_exit[(size_t)k * QW + (q >> 5)] >> (q & 31)) & 1) H.cls_flush[k] |= H.flushlab[q];
+
+  // ---------------------------------------------------------------- gap derivations
+  // Inside a masked run the class nodes and their edges do not depend on the
+  // sequence, so what the run can derive does not either.  eps_path[j*K+k]:
+  // class k is reachable from class j by epsilon edges (reflexive).
+  // gap_nt[j*K+k]: nonterminals B with a string of L(B) labelling a path from
+  // class j to class k (least fixpoint over the productions, the Bar-Hillel
+  // construction restricted to the run's class automaton).
+  const int KK = std::max(K, 1);
+  std::vector<char> epsp((size_t)KK * KK, 0);
+  for (int j = 0; j < K; ++j) epsp[(size_t)j * K + j] = 1;
+  for (bool changed = true; changed;) {
+    changed = false;
+    for (int i = 0; i < K; ++i)
+      for (int j = 0; j < K; ++j)
+        if (epsp[(size_t)i * K + j])
+          for (int k = 0; k < K; ++k)
+            if (((H.cls_internal[(size_t)j * K + k] >> kLabelEps) & 1) && !epsp[(size_t)i * K + k]) {
+              epsp[(size_t)i * K + k] = 1;
+              changed = true;
+            }
+  }
+  std::vector<uint64_t> gnt((size_t)KK * KK, 0);
+  for (bool changed = true; changed;) {
+    changed = false;
+    for (int p = 0; p < P; ++p) {
+      const int A = lhs[p] - T;
+      for (int j = 0; j < K; ++j) {
+        std::vector<char> S(K, 0);
+        for (int k = 0; k < K; ++k) S[k] = epsp[(size_t)j * K + k];
+        for (int i = roff[p]; i < roff[p + 1]; ++i) {
+          const int X = rhs[i];
+          std::vector<char> S2(K, 0);
+          for (int c = 0; c < K; ++c) {
+            if (!S[c]) continue;
+            for (int c2 = 0; c2 < K; ++c2) {
+              if (X < T) {
+                if ((H.cls_internal[(size_t)c * K + c2] >> X) & 1)
+                  for (int c3 = 0; c3 < K; ++c3)
+                    if (epsp[(size_t)c2 * K + c3]) S2[c3] = 1;
+              } else if ((gnt[(size_t)c * K + c2] >> (X - T)) & 1) {
+                S2[c2] = 1;
+              }
+            }
+          }
+          S = S2;
+        }
+        for (int k = 0; k < K; ++k)
+          if (S[k] && !((gnt[(size_t)j * K + k] >> A) & 1)) {
+            gnt[(size_t)j * K + k] |= 1ull << A;
+            changed = true;
+          }
+      }
+    }
+  }
+  // transfer masks between the class nodes of a run: items whose next symbol
+  // is a label of an edge j -> k or a nonterminal derivable from j to k
+  H.gap_eps = 0;
+  H.gap_tm.assign((size_t)KK * KK * W, 0);
+  for (int j = 0; j < K; ++j)
+    for (int k = 0; k < K; ++k) {
+      if (epsp[(size_t)j * K + k]) H.gap_eps |= 1ull << (j * K + k);
+      Set m = exp_mask(gnt[(size_t)j * K + k]);
+      uint64_t lab = H.cls_internal[(size_t)j * K + k] & ~(1ull << kLabelEps);
+      for (int a = 0; a < T; ++a)
+        if ((lab >> a) & 1)
+          for (int w = 0; w < W; ++w) m[w] |= H.exp_t[(size_t)a * W + w];
+      for (int w = 0; w < W; ++w) H.gap_tm[((size_t)j * K + k) * W + w] = m[w];
+    }
+  H.gap_nt = gnt;
+  // Entries of a run's own origins: every production predicted at class node
+  // j (predicting everything is sound: an Earley item only asserts that its
+  // prefix derives the input it spans), closed under the run's transfers;
+  // gap_own[(j*K + k)*W ..] is the item set of the entry of origin j at class k.
+  H.gap_own.assign((size_t)KK * KK * W, 0);
+  for (int j = 0; j < K; ++j) {
+    std::vector<Set> x(K, Set(W, 0));
+    for (int A = 0; A < N; ++A)
+      for (int w = 0; w < W; ++w) x[j][w] |= H.start_of[(size_t)A * W + w];
+    for (bool changed = true; changed;) {
+      changed = false;
+      for (int a = 0; a < K; ++a)
+        for (int b = 0; b < K; ++b) {
+          Set m(H.gap_tm.begin() + ((size_t)a * K + b) * W, H.gap_tm.begin() + ((size_t)a * K + b + 1) * W);
+          if (adv_or(x[a], m, x[b])) changed = true;
+          if (a != b && epsp[(size_t)a * K + b])
+            for (int w = 0; w < W; ++w)
+              if (x[a][w] & ~x[b][w]) {
+                x[b][w] |= x[a][w];
+                changed = true;
+              }
+        }
+    }
+    for (int k = 0; k < K; ++k)
+      for (int w = 0; w < W; ++w) H.gap_own[((size_t)j * K + k) * W + w] = x[k][w];
+  }
   return 0;
 }
 

@@ -31,13 +31,21 @@ struct HostTables {
   std::vector<uint64_t> cls_internal;   // [K*K] labels of edges class k -> class k'
   std::vector<uint64_t> cls_entry;      // [Q*K] labels of edges from an entry lexeme in state q into class k
   std::vector<uint64_t> cls_flush;      // [K]
+  // what a masked run derives between its class nodes (independent of the sequence)
+  std::vector<uint64_t> gap_nt;   // [K*K] nonterminals deriving a path from class j to class k
+  uint64_t gap_eps = 0;           // bit j*K+k: class k reachable from class j by epsilon edges
+  std::vector<uint32_t> gap_tm;   // [K*K*W] items that advance from class j to class k
+  std::vector<uint32_t> gap_own;  // [K*K*W] entry of the run's origin j at class k
   // grammar (dotted items numbered per production, consecutively)
   std::vector<uint32_t> exp_t;     // [T*W] items whose next symbol is terminal a
   std::vector<uint32_t> exp_n;     // [N*W] items whose next symbol is nonterminal B
-  std::vector<uint32_t> pred;      // [N*W] items B' -> . gamma for B' in the left-corner closure of B
+  std::vector<uint32_t> pred;      // [N*W] prediction closure of B (nullable nonterminals skipped)
   std::vector<uint32_t> complete;  // [W] items with the dot at the end (augmented item excluded)
   std::vector<int8_t> item_lhs;    // [NI] nonterminal index of the item's production (-1: augmented)
   std::vector<int8_t> next_nt;     // [NI] nonterminal index after the dot (-1: terminal or end)
+  std::vector<int8_t> next_sym;    // [NI] symbol after the dot: terminal a, 64 + nonterminal B, -1 at the end
+  uint64_t nullable = 0;           // nonterminals deriving the empty string
+  std::vector<uint32_t> mn;        // [W] items whose next symbol is a nullable nonterminal
   std::vector<uint32_t> start_of;  // [N*W] items A -> . gamma
   std::vector<uint32_t> end_of;    // [N*W] items A -> gamma .
   // regular cover: state bit i < 32W is dotted item i (rule position), bit 32W+A is
