@@ -53,10 +53,11 @@ __device__ inline uint64_t grp_or64(uint64_t v, int G) {
 
 #include "walker.inc"
 
-// Threads per walk: one lane group of W lanes per chart entry; wide item sets
-// (W = 16) get 32 groups, narrow ones 64 to 256.
+// Threads per walk: one lane group of W lanes per chart entry; 512 threads
+// are two wavefronts per SIMD, which hides part of the memory latency of
+// the chart reads.
 template <int W>
-constexpr int threads_for() { return W >= 16 ? 512 : 256; }
+constexpr int threads_for() { return 512; }
 constexpr int kMemoThreads = 256;
 
 // ------------------------------------------------------------------ memo
@@ -433,6 +434,7 @@ epic_status upload(epic_ctx* c) {
          o_expn = place(blob, H.exp_n), o_pred = place(blob, H.pred), o_comp = place(blob, H.complete),
          o_lhs = place(blob, H.item_lhs), o_nsym = place(blob, H.next_sym), o_mn = place(blob, H.mn),
          o_gtm = place(blob, H.gap_tm), o_gown = place(blob, H.gap_own), o_ccl = place(blob, H.cover_cl),
+         o_enib = place(blob, H.expn_nib), o_pnib = place(blob, H.pred_nib),
          o_vb = place(blob, H.vbytes), o_vo = place(blob, H.voffs);
   if (hipMalloc(&c->d_tables, blob.size()) != hipSuccess) return EPIC_ERR_HIP;
   if (hipMemcpy(c->d_tables, blob.data(), blob.size(), hipMemcpyHostToDevice) != hipSuccess) return EPIC_ERR_HIP;
@@ -471,6 +473,8 @@ epic_status upload(epic_ctx* c) {
   t.gap_tm = (const uint32_t*)(d + o_gtm);
   t.gap_own = (const uint32_t*)(d + o_gown);
   t.gap_eps = H.gap_eps;
+  t.expn_nib = (const uint32_t*)(d + o_enib);
+  t.pred_nib = (const uint32_t*)(d + o_pnib);
   t.cover_cl = (const uint32_t*)(d + o_ccl);
   t.vbytes = (const uint8_t*)(d + o_vb);
   t.voffs = (const int32_t*)(d + o_vo);

@@ -280,6 +280,18 @@ int build_tables(int Q, const int16_t* trans, const int16_t* accept, int T, int 
     }
     for (int w = 0; w < W; ++w) H.pred[(size_t)B * W + w] = x[w];
   }
+  H.expn_nib.assign((size_t)16 * 16 * W, 0);
+  H.pred_nib.assign((size_t)16 * 16 * W, 0);
+  for (int i = 0; i < 16; ++i)
+    for (int v = 0; v < 16; ++v)
+      for (int b = 0; b < 4; ++b) {
+        const int B = 4 * i + b;
+        if (!((v >> b) & 1) || B >= N) continue;
+        for (int w = 0; w < W; ++w) {
+          H.expn_nib[((size_t)i * 16 + v) * W + w] |= H.exp_n[(size_t)B * W + w];
+          H.pred_nib[((size_t)i * 16 + v) * W + w] |= H.pred[(size_t)B * W + w];
+        }
+      }
 
   // ---------------------------------------------------------------- cover
   {

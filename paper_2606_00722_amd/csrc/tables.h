@@ -46,6 +46,10 @@ struct HostTables {
   std::vector<int8_t> next_sym;    // [NI] symbol after the dot: terminal a, 64 + nonterminal B, -1 at the end
   uint64_t nullable = 0;           // nonterminals deriving the empty string
   std::vector<uint32_t> mn;        // [W] items whose next symbol is a nullable nonterminal
+  // nibble-indexed unions: expn_nib[((i*16 + v)*W ..] = union of exp_n[B] over
+  // the nonterminals B = 4i + b with bit b of v set; pred_nib likewise for pred
+  std::vector<uint32_t> expn_nib;  // [16*16*W]
+  std::vector<uint32_t> pred_nib;  // [16*16*W]
   std::vector<uint32_t> start_of;  // [N*W] items A -> . gamma
   std::vector<uint32_t> end_of;    // [N*W] items A -> gamma .
   // regular cover: state bit i < 32W is dotted item i (rule position), bit 32W+A is
