@@ -434,7 +434,7 @@ epic_status upload(epic_ctx* c) {
          o_expn = place(blob, H.exp_n), o_pred = place(blob, H.pred), o_comp = place(blob, H.complete),
          o_lhs = place(blob, H.item_lhs), o_nsym = place(blob, H.next_sym), o_mn = place(blob, H.mn),
          o_gtm = place(blob, H.gap_tm), o_gown = place(blob, H.gap_own), o_ccl = place(blob, H.cover_cl),
-         o_enib = place(blob, H.expn_nib), o_pnib = place(blob, H.pred_nib),
+         o_enib = place(blob, H.expn_nib), o_pnib = place(blob, H.pred_nib), o_gcov = place(blob, H.gap_cover),
          o_vb = place(blob, H.vbytes), o_vo = place(blob, H.voffs);
   if (hipMalloc(&c->d_tables, blob.size()) != hipSuccess) return EPIC_ERR_HIP;
   if (hipMemcpy(c->d_tables, blob.data(), blob.size(), hipMemcpyHostToDevice) != hipSuccess) return EPIC_ERR_HIP;
@@ -475,6 +475,7 @@ epic_status upload(epic_ctx* c) {
   t.gap_eps = H.gap_eps;
   t.expn_nib = (const uint32_t*)(d + o_enib);
   t.pred_nib = (const uint32_t*)(d + o_pnib);
+  t.gap_cover = (const uint32_t*)(d + o_gcov);
   t.cover_cl = (const uint32_t*)(d + o_ccl);
   t.vbytes = (const uint8_t*)(d + o_vb);
   t.voffs = (const int32_t*)(d + o_vo);

@@ -546,6 +546,41 @@ int build_tables(int Q, const int16_t* trans, const int16_t* accept, int T, int 
   // j (predicting everything is sound: an Earley item only asserts that its
   // prefix derives the input it spans), closed under the run's transfers;
   // gap_own[(j*K + k)*W ..] is the item set of the entry of origin j at class k.
+  // cover reachability inside a run, by search over (class, cover state)
+  {
+    const int CW = H.CW, S = CW * 32;
+    std::vector<std::vector<int>> ceps(S);
+    for (int s = 0; s < S; ++s)
+      for (int u = 0; u < S; ++u)
+        if (u != s && ((H.cover_cl[(size_t)s * CW + (u >> 5)] >> (u & 31)) & 1)) ceps[s].push_back(u);
+    H.gap_cover.assign((size_t)KK * KK * S * CW, 0);
+    std::vector<char> seen((size_t)KK * S);
+    std::vector<int> stack;
+    for (int j = 0; j < K; ++j)
+      for (int s0 = 0; s0 < S; ++s0) {
+        std::fill(seen.begin(), seen.end(), 0);
+        stack.assign(1, j * S + s0);
+        seen[(size_t)j * S + s0] = 1;
+        while (!stack.empty()) {
+          const int node = stack.back();
+          stack.pop_back();
+          const int c = node / S, st = node % S;
+          H.gap_cover[(((size_t)j * K + c) * S + s0) * CW + (st >> 5)] |= 1u << (st & 31);
+          auto push = [&](int c2, int s2) {
+            if (!seen[(size_t)c2 * S + s2]) {
+              seen[(size_t)c2 * S + s2] = 1;
+              stack.push_back(c2 * S + s2);
+            }
+          };
+          for (int u : ceps[st]) push(c, u);
+          for (int c2 = 0; c2 < K; ++c2) {
+            const uint64_t lab = H.cls_internal[(size_t)c * K + c2];
+            if ((lab >> kLabelEps) & 1) push(c2, st);
+            if (st < ni && H.next_sym[st] >= 0 && H.next_sym[st] < 64 && ((lab >> H.next_sym[st]) & 1)) push(c2, st + 1);
+          }
+        }
+      }
+  }
   H.gap_own.assign((size_t)KK * KK * W, 0);
   for (int j = 0; j < K; ++j) {
     std::vector<Set> x(K, Set(W, 0));

@@ -56,6 +56,10 @@ struct HostTables {
   // the entry state of nonterminal A, bit 32W+64+A its exit state; cover_cl[s] is
   // the epsilon closure of state s (row of CW words, 32*CW rows)
   std::vector<uint32_t> cover_cl;
+  // cover states reachable inside a masked run: gap_cover[((j*K + k)*32*CW + s)*CW ..]
+  // is the set of states at class node k reachable from state s at class node j
+  // (epsilon moves of the cover and the run's own labelled edges)
+  std::vector<uint32_t> gap_cover;
   // vocabulary
   std::vector<uint8_t> vbytes;
   std::vector<int32_t> voffs;
