@@ -42,12 +42,22 @@ __device__ inline uint32_t at_cas32(uint32_t* p, uint32_t cmp, uint32_t val) { r
 __device__ inline int at_min32(int32_t* p, int v) { return atomicMin(p, v); }
 // lane groups: G consecutive lanes of a wavefront (G a power of two <= 64)
 __device__ inline uint32_t grp_shfl(uint32_t v, int src, int G) { return (uint32_t)__shfl((int)v, src, G); }
-__device__ inline uint32_t grp_or32(uint32_t v, int G) {
-  for (int d = 1; d < G; d <<= 1) v |= (uint32_t)__shfl_xor((int)v, d, G);
+// OR over the group by DPP lane permutations within a row of 16 lanes (swap
+// neighbours, swap pairs, mirror each half row, mirror the row); wider groups
+// continue with cross-row shuffles
+template <int G>
+__device__ inline uint32_t grp_or32(uint32_t v) {
+  if constexpr (G >= 2) v |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xF, 0xF, false);
+  if constexpr (G >= 4) v |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, false);
+  if constexpr (G >= 8) v |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x141, 0xF, 0xF, false);
+  if constexpr (G >= 16) v |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x140, 0xF, 0xF, false);
+  if constexpr (G >= 32) v |= (uint32_t)__shfl_xor((int)v, 16, 64);
+  if constexpr (G >= 64) v |= (uint32_t)__shfl_xor((int)v, 32, 64);
   return v;
 }
-__device__ inline uint64_t grp_or64(uint64_t v, int G) {
-  uint32_t lo = grp_or32((uint32_t)v, G), hi = grp_or32((uint32_t)(v >> 32), G);
+template <int G>
+__device__ inline uint64_t grp_or64(uint64_t v) {
+  const uint32_t lo = grp_or32<G>((uint32_t)v), hi = grp_or32<G>((uint32_t)(v >> 32));
   return ((uint64_t)hi << 32) | lo;
 }
 
