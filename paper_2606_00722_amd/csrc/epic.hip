@@ -68,6 +68,7 @@ __device__ inline uint64_t grp_or64(uint64_t v) {
 // the chart reads.
 template <int W>
 constexpr int threads_for() { return 512; }
+
 constexpr int kMemoThreads = 256;
 
 // ------------------------------------------------------------------ memo
