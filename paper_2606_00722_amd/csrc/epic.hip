@@ -201,23 +201,17 @@ __device__ inline void split_halves(uint64_t S, uint64_t& lo, uint64_t& hi) {
   hi = S & ~lo;
 }
 
+// The candidates Alg. 4 selects from for sequence b: its verdict-1
+// candidates, sorted by descending confidence with ties to the lower
+// candidate index, into L.sel_idx/pos/tok/conf (L.sel_n of them).  Clears
+// the sequence's selected flags when `selected` is given.  Returns L.sel_bad:
+// 0 ok, 1 repeated position or NaN confidence, 2 more than 64 candidates,
+// 3 a verdict-1 candidate or a sequence token that is not legal.
 template <int W>
-__global__ void __launch_bounds__(threads_for<W>()) select_kernel(DevTab tb, const int32_t* __restrict__ seqs, int B, int n,
-                                                          const int32_t* __restrict__ cseq,
-                                                          const int32_t* __restrict__ cpos,
-                                                          const int32_t* __restrict__ ctok,
-                                                          const float* __restrict__ conf,
-                                                          const uint8_t* __restrict__ verdict, int C,
-                                                          uint8_t* __restrict__ selected, long long* counts,
-                                                          WsArgs ws) {
-  __shared__ Lds<W> L;
-  __shared__ Frame stack[96];
-  __shared__ int sp;
-  __shared__ uint64_t ret_val, final_B;
-  const int b = blockIdx.x;
-  if (b >= B) return;
-  const WgWork wk = slot_work(ws, blockIdx.x);
-  stage_tables<W>(tb, L);
+__device__ int select_setup(const DevTab& tb, Lds<W>& L, const int32_t* __restrict__ seqs, int n,
+                            const int32_t* __restrict__ cseq, const int32_t* __restrict__ cpos,
+                            const int32_t* __restrict__ ctok, const float* __restrict__ conf,
+                            const uint8_t* __restrict__ verdict, int C, int b, uint8_t* __restrict__ selected) {
   if (threadIdx.x == 0) {
     L.sel_n = 0;
     L.sel_bad = 0;
@@ -225,7 +219,7 @@ __global__ void __launch_bounds__(threads_for<W>()) select_kernel(DevTab tb, con
   __syncthreads();
   for (int c = threadIdx.x; c < C; c += threads_for<W>()) {
     if (cseq[c] != b) continue;
-    selected[c] = 0;
+    if (selected) selected[c] = 0;
     if (verdict[c] != 1) continue;
     const int i = cpos[c], t = ctok[c];
     if (i < 0 || i >= n || t < 0 || t >= tb.V || seqs[(size_t)b * n + i] >= 0) {
@@ -278,6 +272,87 @@ __global__ void __launch_bounds__(threads_for<W>()) select_kernel(DevTab tb, con
           L.sel_conf[j - 1] = tf;
         }
     }
+  }
+  __syncthreads();
+  return L.sel_bad;
+}
+
+// Sequence b with the sorted candidates in mask applied, into L.xtok.
+template <int W>
+__device__ void select_apply(Lds<W>& L, const int32_t* __restrict__ seqs, int n, int b, uint64_t msk) {
+  for (int k = threadIdx.x; k < n; k += threads_for<W>()) L.xtok[k] = seqs[(size_t)b * n + k];
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int i = 0; i < L.sel_n; ++i)
+      if ((msk >> i) & 1) L.xtok[L.sel_pos[i]] = L.sel_tok[i];
+  }
+  __syncthreads();
+}
+
+// Speculated checks: besides its first check (relaxed, on all candidates),
+// the checks Alg. 4 asks for next in the common cases are known before it
+// runs.  Helper workgroups walk them concurrently with the selection and
+// publish each result with a state word (0 not started, 1 running, 2 done,
+// 3 not applicable).  The selection takes a result that is done, waits for
+// one that is running (its helper is resident and finishes on its own), and
+// otherwise walks the check itself.  Check r: r even = relaxed (cover),
+// odd = exact; r < 2 on all sorted candidates, r >= 2 on their
+// high-confidence half (the first ceil(m/2)).
+constexpr int kSpec = 4;
+constexpr long long kSpecWaitCycles = 4ll << 30;  // give up waiting on a helper after this many clocks
+__device__ inline uint64_t spec_mask(int r, int m) {
+  const uint64_t all = m >= 64 ? ~0ull : ((1ull << m) - 1);
+  if (r < 2) return all;
+  uint64_t lo, hi;
+  split_halves(all, lo, hi);
+  return lo;
+}
+
+__global__ void spec_clear_kernel(int32_t* __restrict__ state, int count) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < count) state[i] = 0;
+}
+
+template <int W>
+__global__ void __launch_bounds__(threads_for<W>()) select_kernel(DevTab tb, const int32_t* __restrict__ seqs, int B, int n,
+                                                          const int32_t* __restrict__ cseq,
+                                                          const int32_t* __restrict__ cpos,
+                                                          const int32_t* __restrict__ ctok,
+                                                          const float* __restrict__ conf,
+                                                          const uint8_t* __restrict__ verdict, int C,
+                                                          uint8_t* __restrict__ selected, long long* counts,
+                                                          int32_t* __restrict__ spec, WsArgs ws) {
+  __shared__ Lds<W> L;
+  __shared__ Frame stack[96];
+  __shared__ int sp;
+  __shared__ uint64_t ret_val, final_B;
+  const WgWork wk = slot_work(ws, blockIdx.x);
+  stage_tables<W>(tb, L);
+  int32_t* spec_state = spec;           // [B * kSpec]
+  int32_t* spec_res = spec + B * kSpec;  // [B * kSpec]
+  if ((int)blockIdx.x >= B) {
+    // helper: speculated check r of sequence b
+    const int h = blockIdx.x - B, b = h / (kSpec - 1), r = 1 + h % (kSpec - 1);
+    const int bad = select_setup<W>(tb, L, seqs, n, cseq, cpos, ctok, conf, verdict, C, b, nullptr);
+    const uint64_t msk = spec_mask(r, L.sel_n);
+    if (bad || __popcll(msk) < 2) {  // Alg. 4 checks no subset of one candidate
+      if (threadIdx.x == 0) __hip_atomic_store(&spec_state[b * kSpec + r], 3, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+      return;
+    }
+    if (threadIdx.x == 0) __hip_atomic_store(&spec_state[b * kSpec + r], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    select_apply<W>(L, seqs, n, b, msk);
+    const int res = (r & 1) ? walk<W, W, false>(tb, L, wk, n) : walk<W, W, true>(tb, L, wk, n);
+    if (threadIdx.x == 0) {
+      spec_res[b * kSpec + r] = res < 0 ? -1 : res;  // capacity: the selection walks it again and reports
+      __hip_atomic_store(&spec_state[b * kSpec + r], 2, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    return;
+  }
+  const int b = blockIdx.x;
+  const bool helpers = (int)gridDim.x > B;
+  select_setup<W>(tb, L, seqs, n, cseq, cpos, ctok, conf, verdict, C, b, selected);
+  if (threadIdx.x == 0) {
+    const int m = L.sel_n;
     if (L.sel_bad)
       atomicOr(tb.dev_err, L.sel_bad == 2   ? (uint32_t)EPIC_DEV_CAPACITY
                            : L.sel_bad == 3 ? (uint32_t)EPIC_DEV_BAD_CANDIDATE
@@ -369,20 +444,34 @@ __global__ void __launch_bounds__(threads_for<W>()) select_kernel(DevTab tb, con
     const int req = L.sel_req;
     if (req == kReqDone) break;
     const uint64_t msk = L.sel_mask;
-    for (int k = threadIdx.x; k < n; k += threads_for<W>()) L.xtok[k] = seqs[(size_t)b * n + k];
-    __syncthreads();
-    if (threadIdx.x == 0) {
-      for (int i = 0; i < L.sel_n; ++i)
-        if ((msk >> i) & 1) L.xtok[L.sel_pos[i]] = L.sel_tok[i];
-    }
-    __syncthreads();
-    int r;
-    if (req == kReqCover) {
-      r = walk<W, W, true>(tb, L, wk, n);
+    if (req == kReqCover)
       ++ncover;
-    } else {
-      r = walk<W, W, false>(tb, L, wk, n);
+    else
       ++nexact;
+    int r = -1;
+    if (helpers) {
+      int q = -1;
+      for (int qq = 1; qq < kSpec; ++qq)
+        if (((qq & 1) != 0) == (req == kReqExact) && spec_mask(qq, L.sel_n) == msk) q = qq;
+      if (q > 0 && threadIdx.x == 0) {
+        int res = -1;
+        const long long t_start = (long long)clock64();
+        while ((long long)clock64() - t_start < kSpecWaitCycles) {
+          const int st = __hip_atomic_load(&spec_state[b * kSpec + q], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
+          if (st == 2) res = spec_res[b * kSpec + q];
+          if (st != 1) break;
+          __builtin_amdgcn_s_sleep(8);
+        }
+        L.sel_res = res;
+      }
+      if (q > 0) {
+        __syncthreads();
+        r = L.sel_res;
+      }
+    }
+    if (r < 0) {
+      select_apply<W>(L, seqs, n, b, msk);
+      r = req == kReqCover ? walk<W, W, true>(tb, L, wk, n) : walk<W, W, false>(tb, L, wk, n);
     }
     if (r < 0) {
       failed = true;
@@ -539,8 +628,13 @@ struct SelectLaunch {
   static epic_status run(epic_ctx* c, const int32_t* seqs, int B, int n, const int32_t* cs, const int32_t* cp,
                          const int32_t* ct, const float* conf, const uint8_t* verdict, int C, uint8_t* sel,
                          int64_t* counts, void* ws, hipStream_t stream) {
-    hipLaunchKernelGGL((select_kernel<W>), dim3(B), dim3(threads_for<W>()), 0, stream, c->tab, seqs, B, n, cs, cp, ct, conf,
-                       verdict, C, sel, (long long*)counts, ws_args(c, ws));
+    int32_t* spec = (int32_t*)((char*)ws + c->slot_bytes * c->nslot);
+    // B selection workgroups, then (kSpec - 1) helpers per sequence when the
+    // workspace has chart storage for all of them
+    const int grid = B * kSpec <= c->nslot ? B * kSpec : B;
+    hipLaunchKernelGGL(spec_clear_kernel, dim3((B * kSpec + 255) / 256), dim3(256), 0, stream, spec, B * kSpec);
+    hipLaunchKernelGGL((select_kernel<W>), dim3(grid), dim3(threads_for<W>()), 0, stream,
+                       c->tab, seqs, B, n, cs, cp, ct, conf, verdict, C, sel, (long long*)counts, spec, ws_args(c, ws));
     return hipGetLastError() == hipSuccess ? EPIC_OK : EPIC_ERR_HIP;
   }
 };
@@ -610,7 +704,7 @@ epic_status epic_ctx_create(const epic_lexer_desc* lexer, const epic_grammar_des
   c->off_bits = c->off_st + align256((size_t)c->maxe * 8);
   c->off_cov = c->off_bits + align256((size_t)c->maxe * H.W * 4);
   c->slot_bytes = c->off_cov + align256((size_t)c->maxn * H.CW * 4);
-  c->ws_bytes = c->slot_bytes * c->nslot;
+  c->ws_bytes = c->slot_bytes * c->nslot + align256((size_t)c->max_batch * kSpec * 8);  // + speculated checks
   epic_status s = upload(c);
   if (s != EPIC_OK) {
     epic_ctx_destroy(c);
