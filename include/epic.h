@@ -114,6 +114,11 @@ size_t epic_workspace_bytes(const epic_ctx* ctx);
  * anything else). */
 int32_t epic_gap_classes(const epic_ctx* ctx);
 
+/* Number of 32-bit words of an item bitset (diagnostics; the productions'
+ * dotted items packed so that none straddles a word, rounded up to a power
+ * of two; each chart entry stores this many words). */
+int32_t epic_item_words(const epic_ctx* ctx);
+
 /* Alg. 2, lexing memoization: for every token t and lexer state q the greedy
  * lexing of t's bytes from q, without a final flush, into the context's memo
  * table.  Entry (t, q) sits at byte offset (t*num_states + q)*16:

@@ -726,6 +726,8 @@ size_t epic_workspace_bytes(const epic_ctx* c) { return c ? c->ws_bytes : 0; }
 
 int32_t epic_gap_classes(const epic_ctx* c) { return c ? c->H.K : -1; }
 
+int32_t epic_item_words(const epic_ctx* c) { return c ? c->H.W : -1; }
+
 epic_status epic_lexmemo_build(epic_ctx* c, hipStream_t stream) {
   if (!c) return EPIC_ERR_NULL;
   const size_t total = (size_t)c->H.V * c->H.Q;

@@ -21,7 +21,7 @@ STATUS = {0: "ok", -1: "null pointer", -2: "argument out of range", -3: "capacit
           -7: "HIP runtime error", -8: "memo not built", -9: "unsupported size"}
 DEV_BAD_CANDIDATE, DEV_CAPACITY, DEV_BAD_SELECT = 1, 2, 4
 
-FUNCTIONS = ["epic_ctx_create", "epic_ctx_destroy", "epic_workspace_bytes", "epic_gap_classes",
+FUNCTIONS = ["epic_ctx_create", "epic_ctx_destroy", "epic_workspace_bytes", "epic_gap_classes", "epic_item_words",
              "epic_lexmemo_build", "epic_memo_export", "epic_validate_batch", "epic_select_compatible",
              "epic_ctx_device_error", "epic_ctx_work_counters", "epic_status_string"]
 
@@ -64,6 +64,8 @@ def lib() -> ctypes.CDLL:
         L.epic_workspace_bytes.restype = sz
         L.epic_gap_classes.argtypes = [P]
         L.epic_gap_classes.restype = i32
+        L.epic_item_words.argtypes = [P]
+        L.epic_item_words.restype = i32
         L.epic_lexmemo_build.argtypes = [P, P]
         L.epic_lexmemo_build.restype = ctypes.c_int
         L.epic_memo_export.argtypes = [P, P, sz]
@@ -188,7 +190,8 @@ class Context:
 
     @property
     def item_words(self) -> int:
-        return int(getattr(self, "_item_words", 0))
+        """32-bit words per item bitset of a chart entry."""
+        return int(lib().epic_item_words(self._h))
 
     def device_error(self, stream=None) -> int:
         f = ctypes.c_uint32(0)
