@@ -535,6 +535,7 @@ epic_status upload(epic_ctx* c) {
          o_lhs = place(blob, H.item_lhs), o_nsym = place(blob, H.next_sym), o_mn = place(blob, H.mn),
          o_gtm = place(blob, H.gap_tm), o_gown = place(blob, H.gap_own), o_ccl = place(blob, H.cover_cl),
          o_enib = place(blob, H.expn_nib), o_pnib = place(blob, H.pred_nib), o_gcov = place(blob, H.gap_cover),
+         o_lnib = place(blob, H.lhs_nib), o_snib = place(blob, H.sym_nib),
          o_vb = place(blob, H.vbytes), o_vo = place(blob, H.voffs);
   if (hipMalloc(&c->d_tables, blob.size()) != hipSuccess) return EPIC_ERR_HIP;
   if (hipMemcpy(c->d_tables, blob.data(), blob.size(), hipMemcpyHostToDevice) != hipSuccess) return EPIC_ERR_HIP;
@@ -576,6 +577,8 @@ epic_status upload(epic_ctx* c) {
   t.expn_nib = (const uint32_t*)(d + o_enib);
   t.pred_nib = (const uint32_t*)(d + o_pnib);
   t.gap_cover = (const uint32_t*)(d + o_gcov);
+  t.lhs_nib = (const uint64_t*)(d + o_lnib);
+  t.sym_nib = (const uint64_t*)(d + o_snib);
   t.cover_cl = (const uint32_t*)(d + o_ccl);
   t.vbytes = (const uint8_t*)(d + o_vb);
   t.voffs = (const int32_t*)(d + o_vo);

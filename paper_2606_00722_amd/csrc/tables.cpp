@@ -292,6 +292,22 @@ int build_tables(int Q, const int16_t* trans, const int16_t* accept, int T, int 
           H.pred_nib[((size_t)i * 16 + v) * W + w] |= H.pred[(size_t)B * W + w];
         }
       }
+  H.lhs_nib.assign((size_t)W * 8 * 16, 0);
+  H.sym_nib.assign((size_t)W * 8 * 16 * 2, 0);
+  for (int w = 0; w < W; ++w)
+    for (int j = 0; j < 8; ++j)
+      for (int v = 0; v < 16; ++v)
+        for (int b = 0; b < 4; ++b) {
+          if (!((v >> b) & 1)) continue;
+          const int it = w * 32 + 4 * j + b;
+          const size_t e = ((size_t)w * 8 + j) * 16 + v;
+          if (((H.complete[w] >> (4 * j + b)) & 1) && H.item_lhs[it] >= 0) H.lhs_nib[e] |= 1ull << H.item_lhs[it];
+          const int sym = H.next_sym[it];
+          if (sym >= 64)
+            H.sym_nib[2 * e] |= 1ull << (sym - 64);
+          else if (sym >= 0)
+            H.sym_nib[2 * e + 1] |= 1ull << sym;
+        }
 
   // ---------------------------------------------------------------- cover
   {

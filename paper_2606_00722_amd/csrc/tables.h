@@ -50,6 +50,11 @@ struct HostTables {
   // the nonterminals B = 4i + b with bit b of v set; pred_nib likewise for pred
   std::vector<uint32_t> expn_nib;  // [16*16*W]
   std::vector<uint32_t> pred_nib;  // [16*16*W]
+  // per item word w and nibble j (bits 4j..4j+3) of it, indexed by the nibble's
+  // value: the nonterminals completed by its end items (lhs_nib), and the
+  // nonterminals and terminals its items expect (sym_nib: pairs of words)
+  std::vector<uint64_t> lhs_nib;  // [W*8*16]
+  std::vector<uint64_t> sym_nib;  // [W*8*16*2]
   std::vector<uint32_t> start_of;  // [N*W] items A -> . gamma
   std::vector<uint32_t> end_of;    // [N*W] items A -> gamma .
   // regular cover: state bit i < 32W is dotted item i (rule position), bit 32W+A is
