@@ -63,12 +63,13 @@ __device__ inline uint64_t grp_or64(uint64_t v) {
 
 #include "walker.inc"
 
-// Threads per walk: one lane group of W lanes per chart entry; 512 threads
-// are two wavefronts per SIMD, which hides part of the memory latency of
-// the chart reads.
-template <int W>
-constexpr int threads_for() { return 512; }
-
+// Threads per walk: two wavefronts per SIMD (512 threads) hide part of the
+// memory latency of the chart reads.  Walks of 16-word item sets, whose rows
+// are the largest, run on 1024 threads when the launch has no more
+// workgroups than the device has CUs (each walk then owns its CU); measured
+// best on the C-like workloads of 256 and 1024 tokens.
+constexpr int kThreads = 512;
+constexpr int kThreadsWide = 1024;
 constexpr int kMemoThreads = 256;
 
 // ------------------------------------------------------------------ memo
@@ -134,8 +135,8 @@ __device__ inline WgWork slot_work(const WsArgs& a, int slot) {
 }
 
 // ------------------------------------------------------------------ validate
-template <int W>
-__global__ void __launch_bounds__(threads_for<W>()) validate_kernel(DevTab tb, const int32_t* __restrict__ seqs, int B,
+template <int W, int NT>
+__global__ void __launch_bounds__(NT) validate_kernel(DevTab tb, const int32_t* __restrict__ seqs, int B,
                                                             int n, const int32_t* __restrict__ cseq,
                                                             const int32_t* __restrict__ cpos,
                                                             const int32_t* __restrict__ ctok, int C,
@@ -155,7 +156,7 @@ __global__ void __launch_bounds__(threads_for<W>()) validate_kernel(DevTab tb, c
     }
     if (threadIdx.x == 0) L.sel_bad = 0;
     __syncthreads();
-    for (int k = threadIdx.x; k < n; k += threads_for<W>()) {
+    for (int k = threadIdx.x; k < n; k += (int)blockDim.x) {
       const int x = k == i ? t : seqs[(size_t)b * n + k];
       if (x < -1 || x >= tb.V) L.sel_bad = 1;
       L.xtok[k] = x;
@@ -217,7 +218,7 @@ __device__ int select_setup(const DevTab& tb, Lds<W>& L, const int32_t* __restri
     L.sel_bad = 0;
   }
   __syncthreads();
-  for (int c = threadIdx.x; c < C; c += threads_for<W>()) {
+  for (int c = threadIdx.x; c < C; c += (int)blockDim.x) {
     if (cseq[c] != b) continue;
     if (selected) selected[c] = 0;
     if (verdict[c] != 1) continue;
@@ -229,7 +230,7 @@ __device__ int select_setup(const DevTab& tb, Lds<W>& L, const int32_t* __restri
     int j = atomicAdd(&L.sel_n, 1);
     if (j < 64) L.sel_idx[j] = c;
   }
-  for (int k = threadIdx.x; k < n; k += threads_for<W>()) {
+  for (int k = threadIdx.x; k < n; k += (int)blockDim.x) {
     const int x = seqs[(size_t)b * n + k];
     if (x < -1 || x >= tb.V) L.sel_bad = 3;
   }
@@ -280,7 +281,7 @@ __device__ int select_setup(const DevTab& tb, Lds<W>& L, const int32_t* __restri
 // Sequence b with the sorted candidates in mask applied, into L.xtok.
 template <int W>
 __device__ void select_apply(Lds<W>& L, const int32_t* __restrict__ seqs, int n, int b, uint64_t msk) {
-  for (int k = threadIdx.x; k < n; k += threads_for<W>()) L.xtok[k] = seqs[(size_t)b * n + k];
+  for (int k = threadIdx.x; k < n; k += (int)blockDim.x) L.xtok[k] = seqs[(size_t)b * n + k];
   __syncthreads();
   if (threadIdx.x == 0) {
     for (int i = 0; i < L.sel_n; ++i)
@@ -313,8 +314,8 @@ __global__ void spec_clear_kernel(int32_t* __restrict__ state, int count) {
   if (i < count) state[i] = 0;
 }
 
-template <int W>
-__global__ void __launch_bounds__(threads_for<W>()) select_kernel(DevTab tb, const int32_t* __restrict__ seqs, int B, int n,
+template <int W, int NT>
+__global__ void __launch_bounds__(NT) select_kernel(DevTab tb, const int32_t* __restrict__ seqs, int B, int n,
                                                           const int32_t* __restrict__ cseq,
                                                           const int32_t* __restrict__ cpos,
                                                           const int32_t* __restrict__ ctok,
@@ -511,6 +512,7 @@ struct epic_ctx {
   DevTab tab{};
   bool memo_built = false;
   int device = 0;
+  int num_cus = 256;
 };
 
 namespace {
@@ -620,8 +622,12 @@ struct ValidateLaunch {
   static epic_status run(epic_ctx* c, const int32_t* seqs, int B, int n, const int32_t* cs, const int32_t* cp,
                          const int32_t* ct, int C, uint8_t* verdict, void* ws, hipStream_t stream) {
     int grid = std::min(C, c->nslot);
-    hipLaunchKernelGGL((validate_kernel<W>), dim3(grid), dim3(threads_for<W>()), 0, stream, c->tab, seqs, B, n, cs, cp, ct,
-                       C, verdict, ws_args(c, ws));
+    if (W >= 16 && grid <= c->num_cus)
+      hipLaunchKernelGGL((validate_kernel<W, kThreadsWide>), dim3(grid), dim3(kThreadsWide), 0, stream, c->tab, seqs, B,
+                         n, cs, cp, ct, C, verdict, ws_args(c, ws));
+    else
+      hipLaunchKernelGGL((validate_kernel<W, kThreads>), dim3(grid), dim3(kThreads), 0, stream, c->tab, seqs, B, n, cs,
+                         cp, ct, C, verdict, ws_args(c, ws));
     return hipGetLastError() == hipSuccess ? EPIC_OK : EPIC_ERR_HIP;
   }
 };
@@ -636,8 +642,12 @@ struct SelectLaunch {
     // workspace has chart storage for all of them
     const int grid = B * kSpec <= c->nslot ? B * kSpec : B;
     hipLaunchKernelGGL(spec_clear_kernel, dim3((B * kSpec + 255) / 256), dim3(256), 0, stream, spec, B * kSpec);
-    hipLaunchKernelGGL((select_kernel<W>), dim3(grid), dim3(threads_for<W>()), 0, stream,
-                       c->tab, seqs, B, n, cs, cp, ct, conf, verdict, C, sel, (long long*)counts, spec, ws_args(c, ws));
+    if (W >= 16 && grid <= c->num_cus)
+      hipLaunchKernelGGL((select_kernel<W, kThreadsWide>), dim3(grid), dim3(kThreadsWide), 0, stream, c->tab, seqs, B,
+                         n, cs, cp, ct, conf, verdict, C, sel, (long long*)counts, spec, ws_args(c, ws));
+    else
+      hipLaunchKernelGGL((select_kernel<W, kThreads>), dim3(grid), dim3(kThreads), 0, stream, c->tab, seqs, B, n, cs,
+                         cp, ct, conf, verdict, C, sel, (long long*)counts, spec, ws_args(c, ws));
     return hipGetLastError() == hipSuccess ? EPIC_OK : EPIC_ERR_HIP;
   }
 };
@@ -692,6 +702,9 @@ epic_status epic_ctx_create(const epic_lexer_desc* lexer, const epic_grammar_des
     return (epic_status)r;
   }
   if (hipGetDevice(&c->device) != hipSuccess) c->device = 0;
+  if (hipDeviceGetAttribute(&c->num_cus, hipDeviceAttributeMultiprocessorCount, c->device) != hipSuccess ||
+      c->num_cus < 1)
+    c->num_cus = 256;
   c->max_batch = max_batch;
   c->max_seq = max_seq_len;
   c->max_cands = max_cands;

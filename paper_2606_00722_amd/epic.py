@@ -14,7 +14,8 @@ from typing import Optional
 import numpy as np
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libepic.so")
+# EPIC_LIB names another build of the same library (e.g. a profiling build)
+LIB_PATH = os.environ.get("EPIC_LIB") or os.path.join(HERE, "libepic.so")
 
 STATUS = {0: "ok", -1: "null pointer", -2: "argument out of range", -3: "capacity exceeded",
           -4: "malformed lexer DFA", -5: "malformed grammar", -6: "malformed vocabulary",
