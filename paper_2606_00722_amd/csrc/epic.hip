@@ -112,11 +112,15 @@ __global__ void __launch_bounds__(kMemoThreads) lexmemo_kernel(DevTab tb, uint4*
   memo[i] = e;
 }
 
+// Workspace: nslot chart slots for walks, then base_slots chart slots for
+// the base walks of prefix sharing (one per sequence), then one snapshot
+// record per base slot.
 struct WsArgs {
   char* base;
   size_t slot_bytes;
   size_t off_cnt, off_org, off_sn, off_st, off_bits, off_cov;
-  int maxn, maxe;
+  int maxn, maxe, nslot;
+  size_t snap_off, snap_bytes;
 };
 
 __device__ inline WgWork slot_work(const WsArgs& a, int slot) {
@@ -131,11 +135,87 @@ __device__ inline WgWork slot_work(const WsArgs& a, int slot) {
   w.cov = (uint32_t*)(b + a.off_cov);
   w.maxn = a.maxn;
   w.maxe = a.maxe;
+  w.b_row_off = w.row_off;
+  w.b_row_cnt = w.row_cnt;
+  w.b_ent_org = w.ent_org;
+  w.b_ent_sn = w.ent_sn;
+  w.b_ent_st = w.ent_st;
+  w.b_ent_bits = w.ent_bits;
+  w.b_cov = w.cov;
+  w.split_node = 0;
+  w.split_ent = 0;
   return w;
+}
+__device__ inline char* snap_record(const WsArgs& a, int b) { return a.base + a.snap_off + (size_t)b * a.snap_bytes; }
+
+// Resume walk for sequence b at token i0 from its base walk: load the
+// snapshot of masked run `run` into LDS (frontier in buffer 0, node
+// counters, row mirrors of the shared nodes) and point w's reads of the
+// shared prefix at the base chart.
+template <int W>
+__device__ void resume_from_base(Lds<W>& L, const WsArgs& a, int b, int run, WgWork& w) {
+  const WgWork base = slot_work(a, a.nslot + b);
+  const Snapshot* sp = reinterpret_cast<const Snapshot*>(snap_record(a, b) + kSnapHeader) + run;
+  const int t0 = threadIdx.x, NT = blockDim.x;
+  const int nn = sp->next_node, ne = sp->ent_cursor, nf = sp->fr_n;
+  if (t0 == 0) {
+    L.next_node = nn;
+    L.ent_cursor = ne;
+    L.fr_n[0] = nf;
+  }
+  for (int i = t0; i < nf * (kQW + 1); i += NT) {
+    const int f = i / (kQW + 1), q = i % (kQW + 1);
+    if (q == kQW)
+      L.fr_node[0][f] = sp->fr_node[f];
+    else
+      L.fr_set[0][f][q] = sp->fr_set[f][q];
+  }
+  const int nc = nn < Lds<W>::kNodeCache ? nn : Lds<W>::kNodeCache;
+  for (int v = t0; v < nc; v += NT) {
+    const int c = base.row_cnt[v];
+    L.n_off[v] = base.row_off[v];
+    L.n_cnt[v] = (int16_t)((c & kCntMask) | ((c & kOwnFlag) ? 0x8000 : 0));
+  }
+  w.b_row_off = base.row_off;
+  w.b_row_cnt = base.row_cnt;
+  w.b_ent_org = base.ent_org;
+  w.b_ent_sn = base.ent_sn;
+  w.b_ent_st = base.ent_st;
+  w.b_ent_bits = base.ent_bits;
+  w.b_cov = base.cov;
+  w.split_node = nn;
+  w.split_ent = ne;
+  __syncthreads();
+}
+
+// Base walks: sequence b (= blockIdx.x) as given, recording its state at
+// every masked run, in chart slot nslot + b.
+template <int W, int NT>
+__global__ void __launch_bounds__(NT) base_kernel(DevTab tb, const int32_t* __restrict__ seqs, int B, int n,
+                                                  WsArgs ws) {
+  __shared__ Lds<W> L;
+  const int b = blockIdx.x;
+  if (b >= B) return;
+  const WgWork wk = slot_work(ws, ws.nslot + b);
+  stage_tables<W>(tb, L);
+  if (threadIdx.x == 0) L.sel_bad = 0;
+  __syncthreads();
+  for (int k = threadIdx.x; k < n; k += NT) {
+    const int x = seqs[(size_t)b * n + k];
+    if (x < -1 || x >= tb.V) L.sel_bad = 1;
+    L.xtok[k] = x;
+  }
+  __syncthreads();
+  char* snap = snap_record(ws, b);
+  if (L.sel_bad) {  // an illegal token: no snapshot, candidates report it themselves
+    record_end(L, snap, 2, 0);
+    return;
+  }
+  walk<W, W, false>(tb, L, wk, n, 0, false, snap);
 }
 
 // ------------------------------------------------------------------ validate
-template <int W, int NT>
+template <int W, int NT, bool SHARE>
 __global__ void __launch_bounds__(NT) validate_kernel(DevTab tb, const int32_t* __restrict__ seqs, int B,
                                                             int n, const int32_t* __restrict__ cseq,
                                                             const int32_t* __restrict__ cpos,
@@ -170,7 +250,35 @@ __global__ void __launch_bounds__(NT) validate_kernel(DevTab tb, const int32_t* 
       __syncthreads();
       continue;
     }
-    const int r = walk<W, W, false>(tb, L, wk, n);
+    int r;
+    if (SHARE) {
+      // the masked run of x_b holding position i: its start p0 and ordinal
+      if (threadIdx.x == 0) {
+        L.minp = -1;  // last fixed position before i
+        L.rep_b = 0;  // masked runs starting before p0
+      }
+      __syncthreads();
+      for (int k = threadIdx.x; k < i; k += NT)
+        if (L.xtok[k] >= 0) atomicMax(&L.minp, k);
+      __syncthreads();
+      const int p0 = L.minp + 1;
+      for (int k = threadIdx.x; k < p0; k += NT)
+        if (L.xtok[k] < 0 && (k == 0 || L.xtok[k - 1] >= 0)) atomicAdd(&L.rep_b, 1);
+      __syncthreads();
+      const int run = L.rep_b;
+      const int32_t* h = reinterpret_cast<const int32_t*>(snap_record(ws, b));
+      const int status = h[0], runs = h[1];
+      if (run < runs) {
+        WgWork wr = wk;
+        resume_from_base<W>(L, ws, b, run, wr);
+        r = walk<W, W, false>(tb, L, wr, n, p0, true);
+      } else {
+        r = status == 1 ? 0 : -1;  // the shared prefix died, or overflowed
+        if (threadIdx.x == 0 && r < 0) L.overflow = kOvEntries;
+      }
+    } else {
+      r = walk<W, W, false>(tb, L, wk, n);
+    }
     if (threadIdx.x == 0) {
       verdict[c] = (uint8_t)(r < 0 ? 2 : r);
       if (r < 0) atomicOr(tb.dev_err, (uint32_t)EPIC_DEV_CAPACITY | (1u << (8 + (L.overflow & 15))));
@@ -513,6 +621,8 @@ struct epic_ctx {
   bool memo_built = false;
   int device = 0;
   int num_cus = 256;
+  int base_slots = 0;
+  size_t off_snap = 0, snap_bytes = 0, off_spec = 0;
 };
 
 namespace {
@@ -602,6 +712,9 @@ WsArgs ws_args(const epic_ctx* c, void* ws) {
   a.off_cov = c->off_cov;
   a.maxn = c->maxn;
   a.maxe = c->maxe;
+  a.nslot = c->nslot;
+  a.snap_off = c->off_snap;
+  a.snap_bytes = c->snap_bytes;
   return a;
 }
 
@@ -622,12 +735,24 @@ struct ValidateLaunch {
   static epic_status run(epic_ctx* c, const int32_t* seqs, int B, int n, const int32_t* cs, const int32_t* cp,
                          const int32_t* ct, int C, uint8_t* verdict, void* ws, hipStream_t stream) {
     int grid = std::min(C, c->nslot);
-    if (W >= 16 && grid <= c->num_cus)
-      hipLaunchKernelGGL((validate_kernel<W, kThreadsWide>), dim3(grid), dim3(kThreadsWide), 0, stream, c->tab, seqs, B,
-                         n, cs, cp, ct, C, verdict, ws_args(c, ws));
-    else
-      hipLaunchKernelGGL((validate_kernel<W, kThreads>), dim3(grid), dim3(kThreads), 0, stream, c->tab, seqs, B, n, cs,
-                         cp, ct, C, verdict, ws_args(c, ws));
+    const WsArgs wa = ws_args(c, ws);
+    if (grid > c->num_cus && B <= c->base_slots) {
+      // more walks than CUs: the chart up to each candidate's masked run is
+      // its sequence's, walked once by a base walk (prefix sharing)
+      if (W >= 16 && B <= c->num_cus)
+        hipLaunchKernelGGL((base_kernel<W, kThreadsWide>), dim3(B), dim3(kThreadsWide), 0, stream, c->tab, seqs, B, n,
+                           wa);
+      else
+        hipLaunchKernelGGL((base_kernel<W, kThreads>), dim3(B), dim3(kThreads), 0, stream, c->tab, seqs, B, n, wa);
+      hipLaunchKernelGGL((validate_kernel<W, kThreads, true>), dim3(grid), dim3(kThreads), 0, stream, c->tab, seqs, B,
+                         n, cs, cp, ct, C, verdict, wa);
+    } else if (W >= 16 && grid <= c->num_cus) {
+      hipLaunchKernelGGL((validate_kernel<W, kThreadsWide, false>), dim3(grid), dim3(kThreadsWide), 0, stream, c->tab,
+                         seqs, B, n, cs, cp, ct, C, verdict, wa);
+    } else {
+      hipLaunchKernelGGL((validate_kernel<W, kThreads, false>), dim3(grid), dim3(kThreads), 0, stream, c->tab, seqs, B,
+                         n, cs, cp, ct, C, verdict, wa);
+    }
     return hipGetLastError() == hipSuccess ? EPIC_OK : EPIC_ERR_HIP;
   }
 };
@@ -637,7 +762,7 @@ struct SelectLaunch {
   static epic_status run(epic_ctx* c, const int32_t* seqs, int B, int n, const int32_t* cs, const int32_t* cp,
                          const int32_t* ct, const float* conf, const uint8_t* verdict, int C, uint8_t* sel,
                          int64_t* counts, void* ws, hipStream_t stream) {
-    int32_t* spec = (int32_t*)((char*)ws + c->slot_bytes * c->nslot);
+    int32_t* spec = (int32_t*)((char*)ws + c->off_spec);
     // B selection workgroups, then (kSpec - 1) helpers per sequence when the
     // workspace has chart storage for all of them
     const int grid = B * kSpec <= c->nslot ? B * kSpec : B;
@@ -720,7 +845,11 @@ epic_status epic_ctx_create(const epic_lexer_desc* lexer, const epic_grammar_des
   c->off_bits = c->off_st + align256((size_t)c->maxe * 8);
   c->off_cov = c->off_bits + align256((size_t)c->maxe * H.W * 4);
   c->slot_bytes = c->off_cov + align256((size_t)c->maxn * H.CW * 4);
-  c->ws_bytes = c->slot_bytes * c->nslot + align256((size_t)c->max_batch * kSpec * 8);  // + speculated checks
+  c->base_slots = std::min(max_batch, 256);
+  c->snap_bytes = align256(kSnapHeader + (size_t)(max_seq_len / 2 + 1) * sizeof(Snapshot));
+  c->off_snap = c->slot_bytes * (size_t)(c->nslot + c->base_slots);
+  c->off_spec = c->off_snap + c->snap_bytes * c->base_slots;
+  c->ws_bytes = c->off_spec + align256((size_t)c->max_batch * kSpec * 8);  // + speculated checks
   epic_status s = upload(c);
   if (s != EPIC_OK) {
     epic_ctx_destroy(c);

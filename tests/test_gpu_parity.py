@@ -73,6 +73,29 @@ def test_verdicts_full_batch_sampled(preset, sample, gpu_mod, oracle_lib):
     assert np.array_equal(got[idx], want)
 
 
+@pytest.mark.parametrize("preset,reps", [(2, 5), (3, 3), (1, 6)])
+def test_prefix_sharing_bit_exact(preset, reps, gpu_mod, oracle_lib):
+    """More candidates than CUs: each candidate resumes from its sequence's
+    base walk at the start of its masked run.  The step-1 proposals, repeated
+    (with every masked position of the first sequence added, so that
+    candidates sit in the first and the last run), give the same verdicts as
+    the oracle's candidate-by-candidate walks."""
+    inst = W.make_instance(preset, 42)
+    _, g, p = setup(preset, gpu_mod, oracle_lib)
+    pr = W.propose(inst)
+    masked = np.flatnonzero(inst.seqs[0] == W.MASK).astype(np.int32)
+    seq = np.concatenate([np.tile(pr.seq, reps), np.zeros(len(masked), np.int32)])
+    pos = np.concatenate([np.tile(pr.pos, reps), masked])
+    tok = np.concatenate([np.tile(pr.tok, reps), inst.hidden[0, masked].astype(np.int32)])
+    assert len(seq) > 256  # the prefix-sharing launch
+    g2 = gpu_mod.Gpu(W.arrays(inst.lang, inst.vocab), inst.B, inst.n, len(seq))
+    got = g2.validate(inst.seqs, seq, pos, tok)
+    assert g2.errors() == 0
+    want_u = oracle_lib.validate_batch(p, inst.seqs, pr.seq, pr.pos, pr.tok, NTH)
+    want_m = oracle_lib.validate_batch(p, inst.seqs, seq[-len(masked):], pos[-len(masked):], tok[-len(masked):], NTH)
+    assert np.array_equal(got, np.concatenate([np.tile(want_u, reps), want_m]))
+
+
 @pytest.mark.parametrize("preset", [1, 2])
 def test_selection_matches_alg4(preset, gpu_mod, oracle_lib):
     inst = W.make_instance(preset, 42)
