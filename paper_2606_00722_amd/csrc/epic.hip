@@ -70,6 +70,12 @@ __device__ inline uint64_t grp_or64(uint64_t v) {
 // best on the C-like workloads of 256 and 1024 tokens.
 constexpr int kThreads = 512;
 constexpr int kThreadsWide = 1024;
+// Alg. 4 runs several checks per sequence one after another; from this many
+// tokens on, each resumes from base walks of the sequence (prefix sharing).
+#ifndef EPIC_SHARE_SELECT_LEN
+#define EPIC_SHARE_SELECT_LEN 512
+#endif
+constexpr int kShareSelectLen = EPIC_SHARE_SELECT_LEN;
 constexpr int kMemoThreads = 256;
 
 // ------------------------------------------------------------------ memo
@@ -119,7 +125,7 @@ struct WsArgs {
   char* base;
   size_t slot_bytes;
   size_t off_cnt, off_org, off_sn, off_st, off_bits, off_cov;
-  int maxn, maxe, nslot;
+  int maxn, maxe, nslot, base_slots;
   size_t snap_off, snap_bytes;
 };
 
@@ -153,9 +159,9 @@ __device__ inline char* snap_record(const WsArgs& a, int b) { return a.base + a.
 // counters, row mirrors of the shared nodes) and point w's reads of the
 // shared prefix at the base chart.
 template <int W>
-__device__ void resume_from_base(Lds<W>& L, const WsArgs& a, int b, int run, WgWork& w) {
-  const WgWork base = slot_work(a, a.nslot + b);
-  const Snapshot* sp = reinterpret_cast<const Snapshot*>(snap_record(a, b) + kSnapHeader) + run;
+__device__ void resume_from_base(Lds<W>& L, const WsArgs& a, int rec, int run, WgWork& w) {
+  const WgWork base = slot_work(a, a.nslot + rec);
+  const Snapshot* sp = reinterpret_cast<const Snapshot*>(snap_record(a, rec) + kSnapHeader) + run;
   const int t0 = threadIdx.x, NT = blockDim.x;
   const int nn = sp->next_node, ne = sp->ent_cursor, nf = sp->fr_n;
   if (t0 == 0) {
@@ -188,15 +194,19 @@ __device__ void resume_from_base(Lds<W>& L, const WsArgs& a, int b, int run, WgW
   __syncthreads();
 }
 
-// Base walks: sequence b (= blockIdx.x) as given, recording its state at
-// every masked run, in chart slot nslot + b.
+// Base walks: sequence b as given, recording its state at every masked run.
+// Block b < B walks the Earley graph into base record b; with `cover`, block
+// B + b walks the cover graph into base record base_slots + b (the two
+// graphs can differ: a node lives when its row, or its cover set, is not
+// empty).
 template <int W, int NT>
 __global__ void __launch_bounds__(NT) base_kernel(DevTab tb, const int32_t* __restrict__ seqs, int B, int n,
                                                   WsArgs ws) {
   __shared__ Lds<W> L;
-  const int b = blockIdx.x;
-  if (b >= B) return;
-  const WgWork wk = slot_work(ws, ws.nslot + b);
+  const bool cov = (int)blockIdx.x >= B;
+  const int b = cov ? blockIdx.x - B : blockIdx.x;
+  const int rec = cov ? ws.base_slots + b : b;
+  const WgWork wk = slot_work(ws, ws.nslot + rec);
   stage_tables<W>(tb, L);
   if (threadIdx.x == 0) L.sel_bad = 0;
   __syncthreads();
@@ -206,12 +216,15 @@ __global__ void __launch_bounds__(NT) base_kernel(DevTab tb, const int32_t* __re
     L.xtok[k] = x;
   }
   __syncthreads();
-  char* snap = snap_record(ws, b);
+  char* snap = snap_record(ws, rec);
   if (L.sel_bad) {  // an illegal token: no snapshot, candidates report it themselves
     record_end(L, snap, 2, 0);
     return;
   }
-  walk<W, W, false>(tb, L, wk, n, 0, false, snap);
+  if (cov)
+    walk<W, W, true>(tb, L, wk, n, 0, false, snap);
+  else
+    walk<W, W, false>(tb, L, wk, n, 0, false, snap);
 }
 
 // ------------------------------------------------------------------ validate
@@ -398,6 +411,73 @@ __device__ void select_apply(Lds<W>& L, const int32_t* __restrict__ seqs, int n,
   __syncthreads();
 }
 
+// One check of Alg. 4 for sequence b: the walk of x_b with the sorted
+// candidates in msk applied (relaxed: cover graph; exact: Earley graph).
+// With `share`, the walk resumes from the sequence's base walk at the masked
+// run holding the subset's lowest position: x_b and x_b + S agree before it.
+template <int W, bool COVER, bool SHARE>
+__device__ inline int select_walk_body(const DevTab& tb, Lds<W>& L, const WgWork& wk, const WsArgs& ws,
+                           const int32_t* __restrict__ seqs, int n, int b, uint64_t msk) {
+  select_apply<W>(L, seqs, n, b, msk);
+  if constexpr (!SHARE) {
+    return walk<W, W, COVER>(tb, L, wk, n);
+  } else {
+  WgWork wr = wk;
+  int p0 = 0;
+  bool resume = false;
+  {
+    if (threadIdx.x == 0) {
+      int pmin = n;
+      for (int i = 0; i < L.sel_n; ++i)
+        if (((msk >> i) & 1) && L.sel_pos[i] < pmin) pmin = L.sel_pos[i];
+      L.minp = -1;  // last fixed position before pmin
+      L.rep_b = 0;  // masked runs starting before the run of pmin
+      L.result = pmin;
+    }
+    __syncthreads();
+    const int pmin = L.result;
+    for (int k = threadIdx.x; k < pmin; k += blockDim.x)
+      if (L.xtok[k] >= 0) atomicMax(&L.minp, k);
+    __syncthreads();
+    p0 = L.minp + 1;
+    for (int k = threadIdx.x; k < p0; k += blockDim.x)
+      if (L.xtok[k] < 0 && (k == 0 || L.xtok[k - 1] >= 0)) atomicAdd(&L.rep_b, 1);
+    __syncthreads();
+    const int run = L.rep_b, rec = COVER ? ws.base_slots + b : b;
+    const int32_t* h = reinterpret_cast<const int32_t*>(snap_record(ws, rec));
+    const int status = h[0], runs = h[1];
+    if (run >= runs) {
+      if (status == 1) return 0;  // the shared prefix died
+      if (threadIdx.x == 0) L.overflow = kOvEntries;
+      __syncthreads();
+      return -1;
+    }
+    resume_from_base<W>(L, ws, rec, run, wr);
+    resume = true;
+  }
+  return walk<W, W, COVER>(tb, L, wr, n, resume ? p0 : 0, resume);
+  }
+}
+
+// A check walk compiled once per check type (called from the selection and
+// the helper paths): measured faster for 16-word item sets, whose walks are
+// the largest; narrower ones inline it.
+template <int W, bool COVER, bool SHARE>
+__device__ __attribute__((noinline)) int select_walk_call(const DevTab& tb, Lds<W>& L, const WgWork& wk,
+                                                          const WsArgs& ws, const int32_t* __restrict__ seqs, int n,
+                                                          int b, uint64_t msk) {
+  return select_walk_body<W, COVER, SHARE>(tb, L, wk, ws, seqs, n, b, msk);
+}
+
+template <int W, bool COVER, bool SHARE>
+__device__ inline int select_walk(const DevTab& tb, Lds<W>& L, const WgWork& wk, const WsArgs& ws,
+                                  const int32_t* __restrict__ seqs, int n, int b, uint64_t msk) {
+  if constexpr (W >= 16)
+    return select_walk_call<W, COVER, SHARE>(tb, L, wk, ws, seqs, n, b, msk);
+  else
+    return select_walk_body<W, COVER, SHARE>(tb, L, wk, ws, seqs, n, b, msk);
+}
+
 // Speculated checks: besides its first check (relaxed, on all candidates),
 // the checks Alg. 4 asks for next in the common cases are known before it
 // runs.  Helper workgroups walk them concurrently with the selection and
@@ -422,7 +502,7 @@ __global__ void spec_clear_kernel(int32_t* __restrict__ state, int count) {
   if (i < count) state[i] = 0;
 }
 
-template <int W, int NT>
+template <int W, int NT, bool SHARE>
 __global__ void __launch_bounds__(NT) select_kernel(DevTab tb, const int32_t* __restrict__ seqs, int B, int n,
                                                           const int32_t* __restrict__ cseq,
                                                           const int32_t* __restrict__ cpos,
@@ -449,8 +529,8 @@ __global__ void __launch_bounds__(NT) select_kernel(DevTab tb, const int32_t* __
       return;
     }
     if (threadIdx.x == 0) __hip_atomic_store(&spec_state[b * kSpec + r], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    select_apply<W>(L, seqs, n, b, msk);
-    const int res = (r & 1) ? walk<W, W, false>(tb, L, wk, n) : walk<W, W, true>(tb, L, wk, n);
+    const int res = (r & 1) ? select_walk<W, false, SHARE>(tb, L, wk, ws, seqs, n, b, msk)
+                            : select_walk<W, true, SHARE>(tb, L, wk, ws, seqs, n, b, msk);
     if (threadIdx.x == 0) {
       spec_res[b * kSpec + r] = res < 0 ? -1 : res;  // capacity: the selection walks it again and reports
       __hip_atomic_store(&spec_state[b * kSpec + r], 2, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
@@ -578,10 +658,9 @@ __global__ void __launch_bounds__(NT) select_kernel(DevTab tb, const int32_t* __
         r = L.sel_res;
       }
     }
-    if (r < 0) {
-      select_apply<W>(L, seqs, n, b, msk);
-      r = req == kReqCover ? walk<W, W, true>(tb, L, wk, n) : walk<W, W, false>(tb, L, wk, n);
-    }
+    if (r < 0)
+      r = req == kReqCover ? select_walk<W, true, SHARE>(tb, L, wk, ws, seqs, n, b, msk)
+                           : select_walk<W, false, SHARE>(tb, L, wk, ws, seqs, n, b, msk);
     if (r < 0) {
       failed = true;
       break;
@@ -713,6 +792,7 @@ WsArgs ws_args(const epic_ctx* c, void* ws) {
   a.maxn = c->maxn;
   a.maxe = c->maxe;
   a.nslot = c->nslot;
+  a.base_slots = c->base_slots;
   a.snap_off = c->off_snap;
   a.snap_bytes = c->snap_bytes;
   return a;
@@ -766,13 +846,30 @@ struct SelectLaunch {
     // B selection workgroups, then (kSpec - 1) helpers per sequence when the
     // workspace has chart storage for all of them
     const int grid = B * kSpec <= c->nslot ? B * kSpec : B;
+    const WsArgs wa = ws_args(c, ws);
+    // long sequences: Alg. 4's checks resume from base walks of both graphs
+    const int share = n >= kShareSelectLen && B <= c->base_slots;
+    if (share) {
+      if (W >= 16 && 2 * B <= c->num_cus)
+        hipLaunchKernelGGL((base_kernel<W, kThreadsWide>), dim3(2 * B), dim3(kThreadsWide), 0, stream, c->tab, seqs, B,
+                           n, wa);
+      else
+        hipLaunchKernelGGL((base_kernel<W, kThreads>), dim3(2 * B), dim3(kThreads), 0, stream, c->tab, seqs, B, n, wa);
+    }
     hipLaunchKernelGGL(spec_clear_kernel, dim3((B * kSpec + 255) / 256), dim3(256), 0, stream, spec, B * kSpec);
-    if (W >= 16 && grid <= c->num_cus)
-      hipLaunchKernelGGL((select_kernel<W, kThreadsWide>), dim3(grid), dim3(kThreadsWide), 0, stream, c->tab, seqs, B,
-                         n, cs, cp, ct, conf, verdict, C, sel, (long long*)counts, spec, ws_args(c, ws));
+    const bool wide = W >= 16 && grid <= c->num_cus;
+    if (wide && share)
+      hipLaunchKernelGGL((select_kernel<W, kThreadsWide, true>), dim3(grid), dim3(kThreadsWide), 0, stream, c->tab,
+                         seqs, B, n, cs, cp, ct, conf, verdict, C, sel, (long long*)counts, spec, wa);
+    else if (wide)
+      hipLaunchKernelGGL((select_kernel<W, kThreadsWide, false>), dim3(grid), dim3(kThreadsWide), 0, stream, c->tab,
+                         seqs, B, n, cs, cp, ct, conf, verdict, C, sel, (long long*)counts, spec, wa);
+    else if (share)
+      hipLaunchKernelGGL((select_kernel<W, kThreads, true>), dim3(grid), dim3(kThreads), 0, stream, c->tab, seqs, B, n,
+                         cs, cp, ct, conf, verdict, C, sel, (long long*)counts, spec, wa);
     else
-      hipLaunchKernelGGL((select_kernel<W, kThreads>), dim3(grid), dim3(kThreads), 0, stream, c->tab, seqs, B, n, cs,
-                         cp, ct, conf, verdict, C, sel, (long long*)counts, spec, ws_args(c, ws));
+      hipLaunchKernelGGL((select_kernel<W, kThreads, false>), dim3(grid), dim3(kThreads), 0, stream, c->tab, seqs, B,
+                         n, cs, cp, ct, conf, verdict, C, sel, (long long*)counts, spec, wa);
     return hipGetLastError() == hipSuccess ? EPIC_OK : EPIC_ERR_HIP;
   }
 };
@@ -847,8 +944,8 @@ epic_status epic_ctx_create(const epic_lexer_desc* lexer, const epic_grammar_des
   c->slot_bytes = c->off_cov + align256((size_t)c->maxn * H.CW * 4);
   c->base_slots = std::min(max_batch, 256);
   c->snap_bytes = align256(kSnapHeader + (size_t)(max_seq_len / 2 + 1) * sizeof(Snapshot));
-  c->off_snap = c->slot_bytes * (size_t)(c->nslot + c->base_slots);
-  c->off_spec = c->off_snap + c->snap_bytes * c->base_slots;
+  c->off_snap = c->slot_bytes * (size_t)(c->nslot + 2 * c->base_slots);
+  c->off_spec = c->off_snap + c->snap_bytes * 2 * c->base_slots;
   c->ws_bytes = c->off_spec + align256((size_t)c->max_batch * kSpec * 8);  // + speculated checks
   epic_status s = upload(c);
   if (s != EPIC_OK) {
