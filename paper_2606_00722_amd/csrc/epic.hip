@@ -15,6 +15,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cstdio>
 #include <cstring>
 #include <mutex>
@@ -125,8 +126,8 @@ struct WsArgs {
   char* base;
   size_t slot_bytes;
   size_t off_cnt, off_org, off_sn, off_st, off_bits, off_cov;
-  int maxn, maxe, nslot, base_slots;
-  size_t snap_off, snap_bytes;
+  int maxn, maxe, nslot, base_slots, max_seq;
+  size_t snap_off, snap_bytes, bseq_off;
 };
 
 __device__ inline WgWork slot_work(const WsArgs& a, int slot) {
@@ -195,36 +196,70 @@ __device__ void resume_from_base(Lds<W>& L, const WsArgs& a, int rec, int run, W
 }
 
 // Base walks: sequence b as given, recording its state at every masked run.
-// Block b < B walks the Earley graph into base record b; with `cover`, block
-// B + b walks the cover graph into base record base_slots + b (the two
+// Block b < B walks the Earley graph into base record b; block B + b (when
+// launched) walks the cover graph into base record base_slots + b (the two
 // graphs can differ: a node lives when its row, or its cover set, is not
-// empty).
+// empty).  A record left by an earlier call of the same context (owner tag)
+// is reused: the walk state at a masked run depends only on the tokens before
+// it, so the walk resumes at the last recorded run that starts before the
+// first token that differs from the sequence the record was walked on, and
+// a record of the very same sequence is kept as it is.
 template <int W, int NT>
 __global__ void __launch_bounds__(NT) base_kernel(DevTab tb, const int32_t* __restrict__ seqs, int B, int n,
-                                                  WsArgs ws) {
+                                                  uint64_t tag, WsArgs ws) {
   __shared__ Lds<W> L;
   const bool cov = (int)blockIdx.x >= B;
   const int b = cov ? blockIdx.x - B : blockIdx.x;
   const int rec = cov ? ws.base_slots + b : b;
-  const WgWork wk = slot_work(ws, ws.nslot + rec);
+  WgWork wk = slot_work(ws, ws.nslot + rec);
   stage_tables<W>(tb, L);
-  if (threadIdx.x == 0) L.sel_bad = 0;
+  char* snap = snap_record(ws, rec);
+  int32_t* h = reinterpret_cast<int32_t*>(snap);
+  int32_t* walked = reinterpret_cast<int32_t*>(ws.base + ws.bseq_off) + (size_t)rec * ws.max_seq;
+  if (threadIdx.x == 0) {
+    L.sel_bad = 0;
+    L.minp = n;   // first token that differs from the recorded sequence
+    L.rep_b = -1;  // last recorded run starting before it
+  }
   __syncthreads();
+  const bool owned = h[2] >= 0 && h[2] <= ws.max_seq && ((uint64_t)(uint32_t)h[4] | ((uint64_t)(uint32_t)h[5] << 32)) == tag &&
+                     h[1] >= 0 && h[1] <= ws.max_seq / 2 + 1;
+  const int nold = owned ? h[2] : 0;
   for (int k = threadIdx.x; k < n; k += NT) {
     const int x = seqs[(size_t)b * n + k];
     if (x < -1 || x >= tb.V) L.sel_bad = 1;
     L.xtok[k] = x;
+    if (k < nold && walked[k] != x) atomicMin(&L.minp, k);
   }
   __syncthreads();
-  char* snap = snap_record(ws, rec);
   if (L.sel_bad) {  // an illegal token: no snapshot, candidates report it themselves
+    if (threadIdx.x == 0) h[4] = h[5] = 0;  // not reusable
     record_end(L, snap, 2, 0);
     return;
   }
+  int d = L.minp < nold ? L.minp : nold;
+  if (owned && d == n && nold == n) return;  // the record is this sequence's
+  const int runs = owned ? h[1] : 0;
+  const Snapshot* sp0 = reinterpret_cast<const Snapshot*>(snap + kSnapHeader);
+  for (int r = threadIdx.x; r < runs; r += NT)
+    if (sp0[r].start < d) atomicMax(&L.rep_b, r);
+  __syncthreads();
+  const int r0 = L.rep_b;
+  int i0 = 0;
+  if (r0 >= 0) {
+    i0 = sp0[r0].start;
+    resume_from_base<W>(L, ws, rec, r0, wk);  // the record's own chart up to run r0
+  }
+  for (int k = threadIdx.x; k < n; k += NT) walked[k] = L.xtok[k];
+  if (threadIdx.x == 0) {
+    h[2] = n;
+    h[4] = (int32_t)(uint32_t)tag;
+    h[5] = (int32_t)(uint32_t)(tag >> 32);
+  }
   if (cov)
-    walk<W, W, true>(tb, L, wk, n, 0, false, snap);
+    walk<W, W, true>(tb, L, wk, n, i0, r0 >= 0, snap, r0 >= 0 ? r0 : 0);
   else
-    walk<W, W, false>(tb, L, wk, n, 0, false, snap);
+    walk<W, W, false>(tb, L, wk, n, i0, r0 >= 0, snap, r0 >= 0 ? r0 : 0);
 }
 
 // ------------------------------------------------------------------ validate
@@ -701,7 +736,9 @@ struct epic_ctx {
   int device = 0;
   int num_cus = 256;
   int base_slots = 0;
-  size_t off_snap = 0, snap_bytes = 0, off_spec = 0;
+  size_t off_snap = 0, snap_bytes = 0, off_spec = 0, off_bseq = 0;
+  uint64_t tag = 0;  // owner tag of the base records this context writes
+  bool cover_bases = false;  // the last base launch also walked the cover graphs
 };
 
 namespace {
@@ -793,6 +830,8 @@ WsArgs ws_args(const epic_ctx* c, void* ws) {
   a.maxe = c->maxe;
   a.nslot = c->nslot;
   a.base_slots = c->base_slots;
+  a.max_seq = c->max_seq;
+  a.bseq_off = c->off_bseq;
   a.snap_off = c->off_snap;
   a.snap_bytes = c->snap_bytes;
   return a;
@@ -816,14 +855,18 @@ struct ValidateLaunch {
                          const int32_t* ct, int C, uint8_t* verdict, void* ws, hipStream_t stream) {
     int grid = std::min(C, c->nslot);
     const WsArgs wa = ws_args(c, ws);
-    if (grid > c->num_cus && B <= c->base_slots) {
-      // more walks than CUs: the chart up to each candidate's masked run is
-      // its sequence's, walked once by a base walk (prefix sharing)
-      if (W >= 16 && B <= c->num_cus)
-        hipLaunchKernelGGL((base_kernel<W, kThreadsWide>), dim3(B), dim3(kThreadsWide), 0, stream, c->tab, seqs, B, n,
-                           wa);
+    if ((grid > c->num_cus || n >= kShareSelectLen) && B <= c->base_slots) {
+      // more walks than CUs, or long sequences: the chart up to each
+      // candidate's masked run is its sequence's, walked by a base walk
+      // (prefix sharing; long sequences also walk their cover graphs, which
+      // the selection then reuses)
+      const int gb = n >= kShareSelectLen ? 2 * B : B;
+      if (W >= 16 && gb <= c->num_cus)
+        hipLaunchKernelGGL((base_kernel<W, kThreadsWide>), dim3(gb), dim3(kThreadsWide), 0, stream, c->tab, seqs, B, n,
+                           c->tag, wa);
       else
-        hipLaunchKernelGGL((base_kernel<W, kThreads>), dim3(B), dim3(kThreads), 0, stream, c->tab, seqs, B, n, wa);
+        hipLaunchKernelGGL((base_kernel<W, kThreads>), dim3(gb), dim3(kThreads), 0, stream, c->tab, seqs, B, n, c->tag,
+                           wa);
       hipLaunchKernelGGL((validate_kernel<W, kThreads, true>), dim3(grid), dim3(kThreads), 0, stream, c->tab, seqs, B,
                          n, cs, cp, ct, C, verdict, wa);
     } else if (W >= 16 && grid <= c->num_cus) {
@@ -852,9 +895,10 @@ struct SelectLaunch {
     if (share) {
       if (W >= 16 && 2 * B <= c->num_cus)
         hipLaunchKernelGGL((base_kernel<W, kThreadsWide>), dim3(2 * B), dim3(kThreadsWide), 0, stream, c->tab, seqs, B,
-                           n, wa);
+                           n, c->tag, wa);
       else
-        hipLaunchKernelGGL((base_kernel<W, kThreads>), dim3(2 * B), dim3(kThreads), 0, stream, c->tab, seqs, B, n, wa);
+        hipLaunchKernelGGL((base_kernel<W, kThreads>), dim3(2 * B), dim3(kThreads), 0, stream, c->tab, seqs, B, n,
+                           c->tag, wa);
     }
     hipLaunchKernelGGL(spec_clear_kernel, dim3((B * kSpec + 255) / 256), dim3(256), 0, stream, spec, B * kSpec);
     const bool wide = W >= 16 && grid <= c->num_cus;
@@ -945,8 +989,13 @@ epic_status epic_ctx_create(const epic_lexer_desc* lexer, const epic_grammar_des
   c->base_slots = std::min(max_batch, 256);
   c->snap_bytes = align256(kSnapHeader + (size_t)(max_seq_len / 2 + 1) * sizeof(Snapshot));
   c->off_snap = c->slot_bytes * (size_t)(c->nslot + 2 * c->base_slots);
-  c->off_spec = c->off_snap + c->snap_bytes * 2 * c->base_slots;
+  c->off_bseq = c->off_snap + c->snap_bytes * 2 * c->base_slots;
+  c->off_spec = c->off_bseq + align256((size_t)2 * c->base_slots * max_seq_len * 4);
   c->ws_bytes = c->off_spec + align256((size_t)c->max_batch * kSpec * 8);  // + speculated checks
+  {
+    static std::atomic<uint64_t> counter{1};
+    c->tag = (counter.fetch_add(1) << 32) ^ (uint64_t)(uintptr_t)c ^ 0x9E3779B97F4A7C15ull;
+  }
   epic_status s = upload(c);
   if (s != EPIC_OK) {
     epic_ctx_destroy(c);

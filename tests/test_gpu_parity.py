@@ -140,6 +140,25 @@ def test_multistep_evolution(preset, gpu_mod, oracle_lib):
     assert np.array_equal(a.seqs, b.seqs)
 
 
+def test_multistep_prefix_reuse(gpu_mod, oracle_lib):
+    """1024-token sequences decoded in blocks: base walks are reused across
+    calls (each resumes at the last masked run before the first changed
+    token) and by the selection; several steps agree with the oracle."""
+    inst_g = W.make_instance(5, 44, B=6)
+    inst_o = W.make_instance(5, 44, B=6)
+    p = oracle_lib.problem_from(inst_g.lang, inst_g.vocab)
+    g = gpu_mod.Gpu(W.arrays(inst_g.lang, inst_g.vocab), inst_g.B, inst_g.n, inst_g.B * inst_g.cfg["props"])
+    ra = W.run_steps(inst_g, lambda x, pr: g.validate(x, pr.seq, pr.pos, pr.tok),
+                     lambda x, pr, v: g.select(x, pr.seq, pr.pos, pr.tok, pr.conf, v)[0], steps=3)
+    rb = W.run_steps(inst_o, lambda x, pr: oracle_lib.validate_batch(p, x, pr.seq, pr.pos, pr.tok, NTH),
+                     lambda x, pr, v: oracle_lib.select(p, x, pr.seq, pr.pos, pr.tok, pr.conf, v, NTH)[0], steps=3)
+    assert g.errors() == 0
+    for sa, sb in zip(ra, rb):
+        assert np.array_equal(sa.seqs, sb.seqs)
+        assert np.array_equal(sa.verdict, sb.verdict)
+        assert np.array_equal(sa.selected, sb.selected)
+
+
 @pytest.mark.parametrize("name,extra", [("tiny_paren", ["((", "))", "()"]), ("tiny_expr", ["a+", "(a", "a)", " a"]),
                                         ("tiny_kw", ["if", "(x", "x)", " i"]), ("tiny_ab", ["ab", "ba", "cc"]),
                                         ("arith", ["a+", "1*", "(a", " 1"])])
