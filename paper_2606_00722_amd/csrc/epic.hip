@@ -201,9 +201,10 @@ __device__ void resume_from_base(Lds<W>& L, const WsArgs& a, int rec, int run, W
 // graphs can differ: a node lives when its row, or its cover set, is not
 // empty).  A record left by an earlier call of the same context (owner tag)
 // is reused: the walk state at a masked run depends only on the tokens before
-// it, so the walk resumes at the last recorded run that starts before the
-// first token that differs from the sequence the record was walked on, and
-// a record of the very same sequence is kept as it is.
+// it, so the walk resumes at the last recorded run that starts at or before
+// the first token that differs from the sequence the record was walked on
+// (the token there is then walked as the sequence now has it), and a record
+// of the very same sequence is kept as it is.
 template <int W, int NT>
 __global__ void __launch_bounds__(NT) base_kernel(DevTab tb, const int32_t* __restrict__ seqs, int B, int n,
                                                   uint64_t tag, WsArgs ws) {
@@ -242,7 +243,7 @@ __global__ void __launch_bounds__(NT) base_kernel(DevTab tb, const int32_t* __re
   const int runs = owned ? h[1] : 0;
   const Snapshot* sp0 = reinterpret_cast<const Snapshot*>(snap + kSnapHeader);
   for (int r = threadIdx.x; r < runs; r += NT)
-    if (sp0[r].start < d) atomicMax(&L.rep_b, r);
+    if (sp0[r].start <= d) atomicMax(&L.rep_b, r);
   __syncthreads();
   const int r0 = L.rep_b;
   int i0 = 0;
