@@ -105,7 +105,15 @@ epic_status epic_ctx_create(const epic_lexer_desc* lexer, const epic_grammar_des
 void epic_ctx_destroy(epic_ctx* ctx);
 
 /* Bytes of device workspace that epic_validate_batch and
- * epic_select_compatible need (the caller allocates it, 256-byte aligned). */
+ * epic_select_compatible need (the caller allocates it, 256-byte aligned).
+ * Besides per-call scratch the workspace keeps, between calls, the recorded
+ * walks of each sequence (its chart state at every masked run, tagged with the
+ * context and the sequence walked).  A later call on the same context and
+ * workspace resumes a sequence's walk at the last recorded masked run that
+ * starts at or before the first token that changed; any other workspace
+ * contents (fresh, zeroed, another context's) are detected by the tag and
+ * walked from the start.  The caller must not modify the workspace between
+ * calls; results do not depend on its contents, only the time taken does. */
 size_t epic_workspace_bytes(const epic_ctx* ctx);
 
 /* Number of graph nodes one masked run contributes: the left-language
