@@ -27,7 +27,11 @@
 
 namespace epic {
 
-#define EPIC_DEV __device__ inline
+// Device helpers are always inlined: a call that takes a kernel argument or a
+// work descriptor by reference forces it into per-lane scratch memory, and the
+// walks then reload their table pointers from there.
+#define EPIC_DEV __device__ inline __attribute__((always_inline))
+#define EPIC_INLINE EPIC_DEV
 #define EPIC_NOINLINE
 
 __device__ inline int tid() { return (int)threadIdx.x; }
@@ -160,7 +164,7 @@ __device__ inline char* snap_record(const WsArgs& a, int b) { return a.base + a.
 // counters, row mirrors of the shared nodes) and point w's reads of the
 // shared prefix at the base chart.
 template <int W>
-__device__ void resume_from_base(Lds<W>& L, const WsArgs& a, int rec, int run, WgWork& w) {
+EPIC_INLINE void resume_from_base(Lds<W>& L, const WsArgs& a, int rec, int run, WgWork& w) {
   const WgWork base = slot_work(a, a.nslot + rec);
   const Snapshot* sp = reinterpret_cast<const Snapshot*>(snap_record(a, rec) + kSnapHeader) + run;
   const int t0 = threadIdx.x, NT = blockDim.x;
@@ -366,7 +370,7 @@ __device__ inline void split_halves(uint64_t S, uint64_t& lo, uint64_t& hi) {
 // 0 ok, 1 repeated position or NaN confidence, 2 more than 64 candidates,
 // 3 a verdict-1 candidate or a sequence token that is not legal.
 template <int W>
-__device__ int select_setup(const DevTab& tb, Lds<W>& L, const int32_t* __restrict__ seqs, int n,
+EPIC_DEV int select_setup(const DevTab& tb, Lds<W>& L, const int32_t* __restrict__ seqs, int n,
                             const int32_t* __restrict__ cseq, const int32_t* __restrict__ cpos,
                             const int32_t* __restrict__ ctok, const float* __restrict__ conf,
                             const uint8_t* __restrict__ verdict, int C, int b, uint8_t* __restrict__ selected) {
@@ -437,7 +441,7 @@ __device__ int select_setup(const DevTab& tb, Lds<W>& L, const int32_t* __restri
 
 // Sequence b with the sorted candidates in mask applied, into L.xtok.
 template <int W>
-__device__ void select_apply(Lds<W>& L, const int32_t* __restrict__ seqs, int n, int b, uint64_t msk) {
+EPIC_DEV void select_apply(Lds<W>& L, const int32_t* __restrict__ seqs, int n, int b, uint64_t msk) {
   for (int k = threadIdx.x; k < n; k += (int)blockDim.x) L.xtok[k] = seqs[(size_t)b * n + k];
   __syncthreads();
   if (threadIdx.x == 0) {
@@ -452,7 +456,7 @@ __device__ void select_apply(Lds<W>& L, const int32_t* __restrict__ seqs, int n,
 // With `share`, the walk resumes from the sequence's base walk at the masked
 // run holding the subset's lowest position: x_b and x_b + S agree before it.
 template <int W, bool COVER, bool SHARE>
-__device__ inline int select_walk_body(const DevTab& tb, Lds<W>& L, const WgWork& wk, const WsArgs& ws,
+EPIC_INLINE int select_walk_body(const DevTab& tb, Lds<W>& L, const WgWork& wk, const WsArgs& ws,
                            const int32_t* __restrict__ seqs, int n, int b, uint64_t msk) {
   select_apply<W>(L, seqs, n, b, msk);
   if constexpr (!SHARE) {
@@ -495,9 +499,9 @@ __device__ inline int select_walk_body(const DevTab& tb, Lds<W>& L, const WgWork
   }
 }
 
-// A check walk compiled once per check type (called from the selection and
-// the helper paths): measured faster for 16-word item sets, whose walks are
-// the largest; narrower ones inline it.
+// A check walk kept as a function of its own for 16-word item sets: at 1024
+// threads per workgroup (128 registers per lane) it measured faster than the
+// inlined walk, which spills in its inner loops; narrower item sets inline it.
 template <int W, bool COVER, bool SHARE>
 __device__ __attribute__((noinline)) int select_walk_call(const DevTab& tb, Lds<W>& L, const WgWork& wk,
                                                           const WsArgs& ws, const int32_t* __restrict__ seqs, int n,
@@ -506,7 +510,7 @@ __device__ __attribute__((noinline)) int select_walk_call(const DevTab& tb, Lds<
 }
 
 template <int W, bool COVER, bool SHARE>
-__device__ inline int select_walk(const DevTab& tb, Lds<W>& L, const WgWork& wk, const WsArgs& ws,
+EPIC_INLINE int select_walk(const DevTab& tb, Lds<W>& L, const WgWork& wk, const WsArgs& ws,
                                   const int32_t* __restrict__ seqs, int n, int b, uint64_t msk) {
   if constexpr (W >= 16)
     return select_walk_call<W, COVER, SHARE>(tb, L, wk, ws, seqs, n, b, msk);
@@ -555,28 +559,22 @@ __global__ void __launch_bounds__(NT) select_kernel(DevTab tb, const int32_t* __
   stage_tables<W>(tb, L);
   int32_t* spec_state = spec;           // [B * kSpec]
   int32_t* spec_res = spec + B * kSpec;  // [B * kSpec]
-  if ((int)blockIdx.x >= B) {
-    // helper: speculated check r of sequence b
-    const int h = blockIdx.x - B, b = h / (kSpec - 1), r = 1 + h % (kSpec - 1);
-    const int bad = select_setup<W>(tb, L, seqs, n, cseq, cpos, ctok, conf, verdict, C, b, nullptr);
-    const uint64_t msk = spec_mask(r, L.sel_n);
-    if (bad || __popcll(msk) < 2) {  // Alg. 4 checks no subset of one candidate
-      if (threadIdx.x == 0) __hip_atomic_store(&spec_state[b * kSpec + r], 3, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+  // Workgroups b < B run Alg. 4 for sequence b; the others are helpers, each
+  // running one speculated check hr of sequence b.  Both reach the walks
+  // through the one call site of each check type below.
+  const bool helper = (int)blockIdx.x >= B;
+  const int hi = helper ? (int)blockIdx.x - B : 0;
+  const int b = helper ? hi / (kSpec - 1) : (int)blockIdx.x;
+  const int hr = 1 + hi % (kSpec - 1);
+  const bool helpers = (int)gridDim.x > B;
+  const int bad = select_setup<W>(tb, L, seqs, n, cseq, cpos, ctok, conf, verdict, C, b, helper ? nullptr : selected);
+  if (helper) {
+    if (bad || __popcll(spec_mask(hr, L.sel_n)) < 2) {  // Alg. 4 checks no subset of one candidate
+      if (threadIdx.x == 0) __hip_atomic_store(&spec_state[b * kSpec + hr], 3, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
       return;
     }
-    if (threadIdx.x == 0) __hip_atomic_store(&spec_state[b * kSpec + r], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    const int res = (r & 1) ? select_walk<W, false, SHARE>(tb, L, wk, ws, seqs, n, b, msk)
-                            : select_walk<W, true, SHARE>(tb, L, wk, ws, seqs, n, b, msk);
-    if (threadIdx.x == 0) {
-      spec_res[b * kSpec + r] = res < 0 ? -1 : res;  // capacity: the selection walks it again and reports
-      __hip_atomic_store(&spec_state[b * kSpec + r], 2, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
-    }
-    return;
-  }
-  const int b = blockIdx.x;
-  const bool helpers = (int)gridDim.x > B;
-  select_setup<W>(tb, L, seqs, n, cseq, cpos, ctok, conf, verdict, C, b, selected);
-  if (threadIdx.x == 0) {
+    if (threadIdx.x == 0) __hip_atomic_store(&spec_state[b * kSpec + hr], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  } else if (threadIdx.x == 0) {
     const int m = L.sel_n;
     if (L.sel_bad)
       atomicOr(tb.dev_err, L.sel_bad == 2   ? (uint32_t)EPIC_DEV_CAPACITY
@@ -589,14 +587,20 @@ __global__ void __launch_bounds__(NT) select_kernel(DevTab tb, const int32_t* __
     final_B = 0;
   }
   __syncthreads();
-  if (L.sel_bad) return;
+  if (!helper && L.sel_bad) return;
   long long ncover = 0, nexact = 0;
   bool failed = false;
   for (int step = 0; step < 1 << 20; ++step) {
+    int req;
+    uint64_t msk;
+    int r = -1;
+    if (helper) {
+      req = (hr & 1) ? kReqExact : kReqCover;
+      msk = spec_mask(hr, L.sel_n);
+    } else {
     if (threadIdx.x == 0) {
       // run the machine until it needs a check or finishes
       L.sel_req = kReqNone;
-      bool have_ret = false;
       while (L.sel_req == kReqNone) {
         if (sp == 0) {
           L.sel_req = kReqDone;
@@ -662,18 +666,16 @@ __global__ void __launch_bounds__(NT) select_kernel(DevTab tb, const int32_t* __
         ret_val = f.t1 | ret_val;
         --sp;
       }
-      (void)have_ret;
       if (sp >= 95) L.sel_req = kReqDone;  // cannot happen for <= 64 candidates
     }
     __syncthreads();
-    const int req = L.sel_req;
+    req = L.sel_req;
     if (req == kReqDone) break;
-    const uint64_t msk = L.sel_mask;
+    msk = L.sel_mask;
     if (req == kReqCover)
       ++ncover;
     else
       ++nexact;
-    int r = -1;
     if (helpers) {
       int q = -1;
       for (int qq = 1; qq < kSpec; ++qq)
@@ -694,9 +696,17 @@ __global__ void __launch_bounds__(NT) select_kernel(DevTab tb, const int32_t* __
         r = L.sel_res;
       }
     }
+    }
     if (r < 0)
       r = req == kReqCover ? select_walk<W, true, SHARE>(tb, L, wk, ws, seqs, n, b, msk)
                            : select_walk<W, false, SHARE>(tb, L, wk, ws, seqs, n, b, msk);
+    if (helper) {
+      if (threadIdx.x == 0) {
+        spec_res[b * kSpec + hr] = r < 0 ? -1 : r;  // capacity: the selection walks it again and reports
+        __hip_atomic_store(&spec_state[b * kSpec + hr], 2, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+      }
+      return;
+    }
     if (r < 0) {
       failed = true;
       break;
