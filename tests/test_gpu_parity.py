@@ -6,7 +6,7 @@ import pytest
 
 from paper_2606_00722_amd import grammars as G
 from paper_2606_00722_amd import workloads as W
-from tests.util import custom_vocab
+from tests.util import custom_vocab, pad_language
 
 pytestmark = pytest.mark.gpu
 NTH = min(16, os.cpu_count() or 1)
@@ -157,6 +157,29 @@ def test_multistep_prefix_reuse(gpu_mod, oracle_lib):
         assert np.array_equal(sa.seqs, sb.seqs)
         assert np.array_equal(sa.verdict, sb.verdict)
         assert np.array_equal(sa.selected, sb.selected)
+
+
+@pytest.mark.parametrize("preset,words", [(1, 2), (2, 8)])
+def test_padded_grammar_item_widths(preset, words, gpu_mod, oracle_lib):
+    """2- and 8-word item sets, which no workload grammar packs into: the
+    workload's grammar padded with equivalent productions, verdicts and Alg. 4
+    selections against the oracle on the padded grammar, and verdicts equal
+    to the unpadded grammar's (the language is the same)."""
+    inst = W.make_instance(preset, 42)
+    pr = W.propose(inst)
+    lang = pad_language(inst.lang)
+    g = gpu_mod.Gpu(W.arrays(lang, inst.vocab), inst.B, inst.n, max(pr.C, 64))
+    assert g.ctx.item_words == words
+    p = oracle_lib.problem_from(lang, inst.vocab)
+    got = g.validate(inst.seqs, pr.seq, pr.pos, pr.tok)
+    want = oracle_lib.validate_batch(p, inst.seqs, pr.seq, pr.pos, pr.tok, NTH)
+    assert np.array_equal(got, want)
+    p0 = oracle_lib.problem_from(inst.lang, inst.vocab)
+    assert np.array_equal(want, oracle_lib.validate_batch(p0, inst.seqs, pr.seq, pr.pos, pr.tok, NTH))
+    gs, gc = g.select(inst.seqs, pr.seq, pr.pos, pr.tok, pr.conf, want)
+    ws, wc, st = oracle_lib.select(p, inst.seqs, pr.seq, pr.pos, pr.tok, pr.conf, want)
+    assert st == 0 and g.errors() == 0
+    assert np.array_equal(gs, ws) and gc == wc
 
 
 @pytest.mark.parametrize("name,extra", [("tiny_paren", ["((", "))", "()"]), ("tiny_expr", ["a+", "(a", "a)", " a"]),

@@ -33,3 +33,39 @@ def custom_vocab(lang: G.Language, extra: Sequence[str] = ()) -> W.Vocab:
 def encode(vocab: W.Vocab, toks: Sequence[Optional[str]]) -> np.ndarray:
     idx = {s: i for i, s in enumerate(vocab.strings)}
     return np.array([-1 if t is None else idx[t.encode()] for t in toks], dtype=np.int32)
+
+
+def pad_language(lang: G.Language) -> G.Language:
+    """The same language with a larger grammar: every nonterminal A gets a
+    fresh A' with A -> A' and A' -> each right-hand side of A.  L(G) is
+    unchanged (A derives exactly what it did), while the dotted items grow
+    enough to pack into more item words.  Terminals and their ids, hence the
+    lexer, stay as they are."""
+    import dataclasses
+
+    g = lang.grammar
+    extra_nts = [a + "'" for a in g.nonterminals]
+    prods = list(g.productions)
+    for a in g.nonterminals:
+        prods.append((a, (a + "'",)))
+        prods.extend((a + "'", rhs) for lhs, rhs in g.productions if lhs == a)
+    pg = G.Grammar(list(g.terminals), list(g.nonterminals) + extra_nts, prods, g.start)
+    return dataclasses.replace(lang, name=lang.name + "_padded", grammar=pg)
+
+
+def packed_words(g: G.Grammar) -> int:
+    """Item words of a grammar as the library packs it: productions (|rhs|+1
+    items, plus 2 for the augmented start) first-fit by decreasing size into
+    32-bit words, rounded up to a power of two."""
+    bins: List[int] = []
+    for s in sorted([len(r) + 1 for _, r in g.productions] + [2], reverse=True):
+        for i, b in enumerate(bins):
+            if b + s <= 32:
+                bins[i] += s
+                break
+        else:
+            bins.append(s)
+    w = 1
+    while w < len(bins):
+        w *= 2
+    return w
