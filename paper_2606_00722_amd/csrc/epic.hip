@@ -84,6 +84,7 @@ constexpr int kShareSelectLen = EPIC_SHARE_SELECT_LEN;
 constexpr int kMemoThreads = 256;
 
 // ------------------------------------------------------------------ memo
+#ifndef EPIC_KERNEL_UNIT
 __global__ void __launch_bounds__(kMemoThreads) lexmemo_kernel(DevTab tb, uint4* memo) {
   const size_t i = (size_t)blockIdx.x * kMemoThreads + threadIdx.x;
   if (i >= (size_t)tb.V * tb.Q) return;
@@ -122,6 +123,7 @@ __global__ void __launch_bounds__(kMemoThreads) lexmemo_kernel(DevTab tb, uint4*
   }
   memo[i] = e;
 }
+#endif
 
 // Workspace: nslot chart slots for walks, then base_slots chart slots for
 // the base walks of prefix sharing (one per sequence), then one snapshot
@@ -537,6 +539,7 @@ __device__ inline uint64_t spec_mask(int r, int m) {
   return lo;
 }
 
+template <int W>
 __global__ void spec_clear_kernel(int32_t* __restrict__ state, int count) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i < count) state[i] = 0;
@@ -848,6 +851,95 @@ WsArgs ws_args(const epic_ctx* c, void* ws) {
   return a;
 }
 
+}  // namespace
+
+// Launchers of one item width.  Each width's kernels are compiled in a unit of
+// their own (epic_w<W>.hip defines EPIC_KERNEL_UNIT as W and includes this
+// file), so the widths build in parallel; this unit holds the C ABI.
+template <int W>
+struct ValidateLaunch {
+  static epic_status run(epic_ctx* c, const int32_t* seqs, int B, int n, const int32_t* cs, const int32_t* cp,
+                         const int32_t* ct, int C, uint8_t* verdict, void* ws, hipStream_t stream);
+};
+
+template <int W>
+struct SelectLaunch {
+  static epic_status run(epic_ctx* c, const int32_t* seqs, int B, int n, const int32_t* cs, const int32_t* cp,
+                         const int32_t* ct, const float* conf, const uint8_t* verdict, int C, uint8_t* sel,
+                         int64_t* counts, void* ws, hipStream_t stream);
+};
+
+#ifdef EPIC_KERNEL_UNIT
+template <int W>
+epic_status ValidateLaunch<W>::run(epic_ctx* c, const int32_t* seqs, int B, int n, const int32_t* cs,
+                                   const int32_t* cp, const int32_t* ct, int C, uint8_t* verdict, void* ws,
+                                   hipStream_t stream) {
+  int grid = std::min(C, c->nslot);
+  const WsArgs wa = ws_args(c, ws);
+  if ((grid > c->num_cus || n >= kShareSelectLen) && B <= c->base_slots) {
+    // more walks than CUs, or long sequences: the chart up to each
+    // candidate's masked run is its sequence's, walked by a base walk
+    // (prefix sharing; long sequences also walk their cover graphs, which
+    // the selection then reuses)
+    const int gb = n >= kShareSelectLen ? 2 * B : B;
+    if (W >= 16 && gb <= c->num_cus)
+      hipLaunchKernelGGL((base_kernel<W, kThreadsWide>), dim3(gb), dim3(kThreadsWide), 0, stream, c->tab, seqs, B, n,
+                         c->tag, wa);
+    else
+      hipLaunchKernelGGL((base_kernel<W, kThreads>), dim3(gb), dim3(kThreads), 0, stream, c->tab, seqs, B, n, c->tag,
+                         wa);
+    hipLaunchKernelGGL((validate_kernel<W, kThreads, true>), dim3(grid), dim3(kThreads), 0, stream, c->tab, seqs, B,
+                       n, cs, cp, ct, C, verdict, wa);
+  } else if (W >= 16 && grid <= c->num_cus) {
+    hipLaunchKernelGGL((validate_kernel<W, kThreadsWide, false>), dim3(grid), dim3(kThreadsWide), 0, stream, c->tab,
+                       seqs, B, n, cs, cp, ct, C, verdict, wa);
+  } else {
+    hipLaunchKernelGGL((validate_kernel<W, kThreads, false>), dim3(grid), dim3(kThreads), 0, stream, c->tab, seqs, B,
+                       n, cs, cp, ct, C, verdict, wa);
+  }
+  return hipGetLastError() == hipSuccess ? EPIC_OK : EPIC_ERR_HIP;
+}
+
+template <int W>
+epic_status SelectLaunch<W>::run(epic_ctx* c, const int32_t* seqs, int B, int n, const int32_t* cs,
+                                 const int32_t* cp, const int32_t* ct, const float* conf, const uint8_t* verdict,
+                                 int C, uint8_t* sel, int64_t* counts, void* ws, hipStream_t stream) {
+  int32_t* spec = (int32_t*)((char*)ws + c->off_spec);
+  // B selection workgroups, then (kSpec - 1) helpers per sequence when the
+  // workspace has chart storage for all of them
+  const int grid = B * kSpec <= c->nslot ? B * kSpec : B;
+  const WsArgs wa = ws_args(c, ws);
+  // long sequences: Alg. 4's checks resume from base walks of both graphs
+  const int share = n >= kShareSelectLen && B <= c->base_slots;
+  if (share) {
+    if (W >= 16 && 2 * B <= c->num_cus)
+      hipLaunchKernelGGL((base_kernel<W, kThreadsWide>), dim3(2 * B), dim3(kThreadsWide), 0, stream, c->tab, seqs, B,
+                         n, c->tag, wa);
+    else
+      hipLaunchKernelGGL((base_kernel<W, kThreads>), dim3(2 * B), dim3(kThreads), 0, stream, c->tab, seqs, B, n,
+                         c->tag, wa);
+  }
+  hipLaunchKernelGGL(spec_clear_kernel<W>, dim3((B * kSpec + 255) / 256), dim3(256), 0, stream, spec, B * kSpec);
+  const bool wide = W >= 16 && grid <= c->num_cus;
+  if (wide && share)
+    hipLaunchKernelGGL((select_kernel<W, kThreadsWide, true>), dim3(grid), dim3(kThreadsWide), 0, stream, c->tab,
+                       seqs, B, n, cs, cp, ct, conf, verdict, C, sel, (long long*)counts, spec, wa);
+  else if (wide)
+    hipLaunchKernelGGL((select_kernel<W, kThreadsWide, false>), dim3(grid), dim3(kThreadsWide), 0, stream, c->tab,
+                       seqs, B, n, cs, cp, ct, conf, verdict, C, sel, (long long*)counts, spec, wa);
+  else if (share)
+    hipLaunchKernelGGL((select_kernel<W, kThreads, true>), dim3(grid), dim3(kThreads), 0, stream, c->tab, seqs, B, n,
+                       cs, cp, ct, conf, verdict, C, sel, (long long*)counts, spec, wa);
+  else
+    hipLaunchKernelGGL((select_kernel<W, kThreads, false>), dim3(grid), dim3(kThreads), 0, stream, c->tab, seqs, B,
+                       n, cs, cp, ct, conf, verdict, C, sel, (long long*)counts, spec, wa);
+  return hipGetLastError() == hipSuccess ? EPIC_OK : EPIC_ERR_HIP;
+}
+
+template struct ValidateLaunch<EPIC_KERNEL_UNIT>;
+template struct SelectLaunch<EPIC_KERNEL_UNIT>;
+#else
+
 template <template <int> class Launcher, class... Args>
 epic_status dispatch_w(int W, Args... args) {
   switch (W) {
@@ -859,77 +951,6 @@ epic_status dispatch_w(int W, Args... args) {
     default: return EPIC_ERR_UNSUPPORTED;
   }
 }
-
-template <int W>
-struct ValidateLaunch {
-  static epic_status run(epic_ctx* c, const int32_t* seqs, int B, int n, const int32_t* cs, const int32_t* cp,
-                         const int32_t* ct, int C, uint8_t* verdict, void* ws, hipStream_t stream) {
-    int grid = std::min(C, c->nslot);
-    const WsArgs wa = ws_args(c, ws);
-    if ((grid > c->num_cus || n >= kShareSelectLen) && B <= c->base_slots) {
-      // more walks than CUs, or long sequences: the chart up to each
-      // candidate's masked run is its sequence's, walked by a base walk
-      // (prefix sharing; long sequences also walk their cover graphs, which
-      // the selection then reuses)
-      const int gb = n >= kShareSelectLen ? 2 * B : B;
-      if (W >= 16 && gb <= c->num_cus)
-        hipLaunchKernelGGL((base_kernel<W, kThreadsWide>), dim3(gb), dim3(kThreadsWide), 0, stream, c->tab, seqs, B, n,
-                           c->tag, wa);
-      else
-        hipLaunchKernelGGL((base_kernel<W, kThreads>), dim3(gb), dim3(kThreads), 0, stream, c->tab, seqs, B, n, c->tag,
-                           wa);
-      hipLaunchKernelGGL((validate_kernel<W, kThreads, true>), dim3(grid), dim3(kThreads), 0, stream, c->tab, seqs, B,
-                         n, cs, cp, ct, C, verdict, wa);
-    } else if (W >= 16 && grid <= c->num_cus) {
-      hipLaunchKernelGGL((validate_kernel<W, kThreadsWide, false>), dim3(grid), dim3(kThreadsWide), 0, stream, c->tab,
-                         seqs, B, n, cs, cp, ct, C, verdict, wa);
-    } else {
-      hipLaunchKernelGGL((validate_kernel<W, kThreads, false>), dim3(grid), dim3(kThreads), 0, stream, c->tab, seqs, B,
-                         n, cs, cp, ct, C, verdict, wa);
-    }
-    return hipGetLastError() == hipSuccess ? EPIC_OK : EPIC_ERR_HIP;
-  }
-};
-
-template <int W>
-struct SelectLaunch {
-  static epic_status run(epic_ctx* c, const int32_t* seqs, int B, int n, const int32_t* cs, const int32_t* cp,
-                         const int32_t* ct, const float* conf, const uint8_t* verdict, int C, uint8_t* sel,
-                         int64_t* counts, void* ws, hipStream_t stream) {
-    int32_t* spec = (int32_t*)((char*)ws + c->off_spec);
-    // B selection workgroups, then (kSpec - 1) helpers per sequence when the
-    // workspace has chart storage for all of them
-    const int grid = B * kSpec <= c->nslot ? B * kSpec : B;
-    const WsArgs wa = ws_args(c, ws);
-    // long sequences: Alg. 4's checks resume from base walks of both graphs
-    const int share = n >= kShareSelectLen && B <= c->base_slots;
-    if (share) {
-      if (W >= 16 && 2 * B <= c->num_cus)
-        hipLaunchKernelGGL((base_kernel<W, kThreadsWide>), dim3(2 * B), dim3(kThreadsWide), 0, stream, c->tab, seqs, B,
-                           n, c->tag, wa);
-      else
-        hipLaunchKernelGGL((base_kernel<W, kThreads>), dim3(2 * B), dim3(kThreads), 0, stream, c->tab, seqs, B, n,
-                           c->tag, wa);
-    }
-    hipLaunchKernelGGL(spec_clear_kernel, dim3((B * kSpec + 255) / 256), dim3(256), 0, stream, spec, B * kSpec);
-    const bool wide = W >= 16 && grid <= c->num_cus;
-    if (wide && share)
-      hipLaunchKernelGGL((select_kernel<W, kThreadsWide, true>), dim3(grid), dim3(kThreadsWide), 0, stream, c->tab,
-                         seqs, B, n, cs, cp, ct, conf, verdict, C, sel, (long long*)counts, spec, wa);
-    else if (wide)
-      hipLaunchKernelGGL((select_kernel<W, kThreadsWide, false>), dim3(grid), dim3(kThreadsWide), 0, stream, c->tab,
-                         seqs, B, n, cs, cp, ct, conf, verdict, C, sel, (long long*)counts, spec, wa);
-    else if (share)
-      hipLaunchKernelGGL((select_kernel<W, kThreads, true>), dim3(grid), dim3(kThreads), 0, stream, c->tab, seqs, B, n,
-                         cs, cp, ct, conf, verdict, C, sel, (long long*)counts, spec, wa);
-    else
-      hipLaunchKernelGGL((select_kernel<W, kThreads, false>), dim3(grid), dim3(kThreads), 0, stream, c->tab, seqs, B,
-                         n, cs, cp, ct, conf, verdict, C, sel, (long long*)counts, spec, wa);
-    return hipGetLastError() == hipSuccess ? EPIC_OK : EPIC_ERR_HIP;
-  }
-};
-
-}  // namespace
 
 extern "C" {
 
@@ -1098,3 +1119,4 @@ epic_status epic_ctx_device_error(epic_ctx* c, hipStream_t stream, uint32_t* fla
 }
 
 }  // extern "C"
+#endif  // EPIC_KERNEL_UNIT
