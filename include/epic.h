@@ -104,8 +104,8 @@ epic_status epic_ctx_create(const epic_lexer_desc* lexer, const epic_grammar_des
 
 void epic_ctx_destroy(epic_ctx* ctx);
 
-/* Bytes of device workspace that epic_validate_batch and
- * epic_select_compatible need (the caller allocates it, 256-byte aligned).
+/* Bytes of device workspace that epic_validate_batch,
+ * epic_select_compatible and epic_commit_fallback need (the caller allocates it, 256-byte aligned).
  * Besides per-call scratch the workspace keeps, between calls, the recorded
  * walks of each sequence (its chart state at every masked run, tagged with the
  * context and the sequence walked).  A later call on the same context and
@@ -176,6 +176,27 @@ epic_status epic_select_compatible(epic_ctx* ctx, const int32_t* d_seqs, int32_t
                                    const uint8_t* d_verdict, int32_t C, uint8_t* d_selected,
                                    int64_t* d_counts, void* d_workspace, size_t workspace_bytes,
                                    hipStream_t stream);
+
+/* The sequential fallback that follows the relaxed batch in EPIC decoding
+ * (App. E, the decoding algorithm and the paragraph after it): per sequence b,
+ * with the selected set B (d_selected, as written by epic_select_compatible)
+ * committed to x_b, the other candidates of b are taken by descending
+ * confidence (float32, ties to the lower candidate index); each is committed
+ * when x_b + (everything committed so far) + c is valid (Sec. 3 Valid), until
+ * d_num_commit[b] - |B| more are committed (n_t of the step) or the
+ * candidates run out.  Candidates with verdict != 1 are never committed: a
+ * candidate invalid on x_b stays invalid once more masked positions are
+ * filled.  d_num_commit: device int32 [B].  d_accepted: uint8 [C], 1 = the
+ * fallback committed the candidate (B's candidates and the others 0); the
+ * caller applies B and the accepted candidates to x.  Inputs are not
+ * modified.  The same input rules as epic_select_compatible apply: a sequence
+ * whose verdict-1 candidates repeat a position or carry a NaN confidence, or
+ * number more than 64, commits nothing and sets the corresponding flag. */
+epic_status epic_commit_fallback(epic_ctx* ctx, const int32_t* d_seqs, int32_t B, int32_t n,
+                                 const int32_t* d_cand_seq, const int32_t* d_cand_pos, const int32_t* d_cand_tok,
+                                 const float* d_conf, const uint8_t* d_verdict, const uint8_t* d_selected,
+                                 const int32_t* d_num_commit, int32_t C, uint8_t* d_accepted, void* d_workspace,
+                                 size_t workspace_bytes, hipStream_t stream);
 
 /* Synchronise `stream`, then read and clear the sticky device error bits
  * (EPIC_DEV_*) into *flags. */

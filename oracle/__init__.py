@@ -202,3 +202,54 @@ def select(p: Problem, seqs: np.ndarray, seq, pos, tok, conf, verdict, nthreads:
     r = lib().oracle_select(lx, gr, vc, _ptr(s), s.shape[0], s.shape[1], _ptr(cs), _ptr(cp), _ptr(ct), _ptr(cf),
                             _ptr(vd), C, _ptr(out), _ptr(stats), nthreads)
     return out[:C], (int(stats[0]), int(stats[1])), int(r)
+
+
+def fallback(p: Problem, seqs: np.ndarray, seq, pos, tok, conf, verdict, selected, num_commit):
+    """The sequential fallback after the relaxed batch in EPIC decoding (App. E,
+    the decoding algorithm and the paragraph after it), taken step by step:
+    per sequence b, commit the selected set B to x_b, then walk the remaining
+    candidates of b by descending confidence (ties to the lower index) and
+    commit each whose exact check Valid(x_b + c) holds on the current x_b, until
+    num_commit[b] - |B| more are committed or the candidates run out.  Every
+    candidate is checked whatever its verdict; one whose position is no longer
+    masked cannot be applied and is passed over.  Input rules as in `select`: a
+    sequence whose verdict-1 candidates repeat a position or carry a NaN
+    confidence, or number more than 64, commits nothing (status -4 or -2).
+    Returns (accepted uint8[C], status)."""
+    s = np.ascontiguousarray(seqs, dtype=np.int32)
+    cs, cp, ct = _cands(seq, pos, tok)
+    cf = np.asarray(conf, dtype=np.float32)
+    vd = np.asarray(verdict, dtype=np.uint8)
+    sl = np.asarray(selected, dtype=np.uint8)
+    nc = np.asarray(num_commit, dtype=np.int64)
+    C = int(cs.size)
+    acc = np.zeros(C, dtype=np.uint8)
+    status = 0
+    for b in range(s.shape[0]):
+        mine = [c for c in range(C) if cs[c] == b]
+        v1 = [c for c in mine if vd[c] == 1]
+        if any(np.isnan(cf[c]) for c in v1) or len({int(cp[c]) for c in v1}) < len(v1):
+            status = -4
+            continue
+        if len(v1) > 64:
+            status = -2
+            continue
+        x = s[b].copy()
+        committed = [c for c in mine if sl[c]]
+        for c in committed:
+            x[cp[c]] = ct[c]
+        need = int(nc[b]) - len(committed)
+        order = sorted((c for c in mine if not np.isnan(cf[c])), key=lambda c: (-float(cf[c]), c))
+        order += [c for c in mine if np.isnan(cf[c])]
+        for c in order:
+            if need <= 0:
+                break
+            if sl[c] or not (0 <= cp[c] < s.shape[1]) or x[cp[c]] != -1 or not (0 <= ct[c] < len(p.voffs) - 1):
+                continue
+            y = x.copy()
+            y[cp[c]] = ct[c]
+            if valid(p, y) == 1:
+                x = y
+                acc[c] = 1
+                need -= 1
+    return acc, status

@@ -731,6 +731,68 @@ __global__ void __launch_bounds__(NT) select_kernel(DevTab tb, const int32_t* __
   }
 }
 
+// ------------------------------------------------------------------ fallback
+// The sequential fallback that follows the relaxed batch in EPIC decoding
+// (the decoding algorithm of App. E, and the paragraph after it): with the
+// selected set B committed, the remaining candidates of sequence b are taken
+// by descending confidence (ties to the lower candidate index) and each is
+// committed when x + (everything committed so far) + c is valid, until
+// num_commit[b] - |B| more are committed or the candidates run out.  Only
+// verdict-1 candidates are walked: filling masked positions only shrinks the
+// character language of x (a masked run reads any bytes), so a candidate
+// invalid on x stays invalid on every later x.  One workgroup per sequence;
+// the checks are the selection's exact walks.
+template <int W, int NT>
+__global__ void __launch_bounds__(NT) fallback_kernel(DevTab tb, const int32_t* __restrict__ seqs, int B, int n,
+                                                      const int32_t* __restrict__ cseq,
+                                                      const int32_t* __restrict__ cpos,
+                                                      const int32_t* __restrict__ ctok,
+                                                      const float* __restrict__ conf,
+                                                      const uint8_t* __restrict__ verdict,
+                                                      const uint8_t* __restrict__ selected,
+                                                      const int32_t* __restrict__ num_commit, int C,
+                                                      uint8_t* __restrict__ accepted, WsArgs ws) {
+  __shared__ Lds<W> L;
+  __shared__ uint64_t kept;  // sorted candidates committed: B, then the accepted ones
+  __shared__ int need;
+  const WgWork wk = slot_work(ws, blockIdx.x);
+  stage_tables<W>(tb, L);
+  for (int b = blockIdx.x; b < B; b += gridDim.x) {
+    // sorts b's verdict-1 candidates and clears accepted[] of all of b's
+    select_setup<W>(tb, L, seqs, n, cseq, cpos, ctok, conf, verdict, C, b, accepted);
+    if (threadIdx.x == 0) {
+      if (L.sel_bad)
+        atomicOr(tb.dev_err, L.sel_bad == 2   ? (uint32_t)EPIC_DEV_CAPACITY
+                             : L.sel_bad == 3 ? (uint32_t)EPIC_DEV_BAD_CANDIDATE
+                                              : (uint32_t)EPIC_DEV_BAD_SELECT);
+      uint64_t k = 0;
+      for (int i = 0; i < L.sel_n; ++i)
+        if (selected[L.sel_idx[i]]) k |= 1ull << i;
+      kept = k;
+      need = num_commit[b] - __popcll(k);
+    }
+    __syncthreads();
+    if (!L.sel_bad) {
+      for (int i = 0; i < L.sel_n && need > 0; ++i) {
+        if ((kept >> i) & 1) continue;
+        const int r = select_walk<W, false, false>(tb, L, wk, ws, seqs, n, b, kept | (1ull << i));
+        if (r < 0) {
+          if (threadIdx.x == 0)
+            atomicOr(tb.dev_err, (uint32_t)EPIC_DEV_CAPACITY | (1u << (8 + (L.overflow & 15))));
+          break;
+        }
+        if (threadIdx.x == 0 && r) {
+          kept |= 1ull << i;
+          --need;
+          accepted[L.sel_idx[i]] = 1;
+        }
+        __syncthreads();
+      }
+    }
+    __syncthreads();
+  }
+}
+
 }  // namespace epic
 
 // ==================================================================== C ABI
@@ -869,6 +931,13 @@ struct SelectLaunch {
                          int64_t* counts, void* ws, hipStream_t stream);
 };
 
+template <int W>
+struct FallbackLaunch {
+  static epic_status run(epic_ctx* c, const int32_t* seqs, int B, int n, const int32_t* cs, const int32_t* cp,
+                         const int32_t* ct, const float* conf, const uint8_t* verdict, const uint8_t* sel,
+                         const int32_t* num_commit, int C, uint8_t* accepted, void* ws, hipStream_t stream);
+};
+
 #ifdef EPIC_KERNEL_UNIT
 template <int W>
 epic_status ValidateLaunch<W>::run(epic_ctx* c, const int32_t* seqs, int B, int n, const int32_t* cs,
@@ -936,7 +1005,19 @@ epic_status SelectLaunch<W>::run(epic_ctx* c, const int32_t* seqs, int B, int n,
   return hipGetLastError() == hipSuccess ? EPIC_OK : EPIC_ERR_HIP;
 }
 
+template <int W>
+epic_status FallbackLaunch<W>::run(epic_ctx* c, const int32_t* seqs, int B, int n, const int32_t* cs,
+                                   const int32_t* cp, const int32_t* ct, const float* conf, const uint8_t* verdict,
+                                   const uint8_t* sel, const int32_t* num_commit, int C, uint8_t* accepted,
+                                   void* ws, hipStream_t stream) {
+  const int grid = std::min(B, c->nslot);
+  hipLaunchKernelGGL((fallback_kernel<W, kThreads>), dim3(grid), dim3(kThreads), 0, stream, c->tab, seqs, B, n, cs,
+                     cp, ct, conf, verdict, sel, num_commit, C, accepted, ws_args(c, ws));
+  return hipGetLastError() == hipSuccess ? EPIC_OK : EPIC_ERR_HIP;
+}
+
 template struct ValidateLaunch<EPIC_KERNEL_UNIT>;
+template struct FallbackLaunch<EPIC_KERNEL_UNIT>;
 template struct SelectLaunch<EPIC_KERNEL_UNIT>;
 #else
 
@@ -1106,6 +1187,19 @@ epic_status epic_select_compatible(epic_ctx* c, const int32_t* d_seqs, int32_t B
   if (B > c->nslot) return EPIC_ERR_CAPACITY;
   return dispatch_w<SelectLaunch>(c->H.W, c, d_seqs, (int)B, (int)n, d_cand_seq, d_cand_pos, d_cand_tok, d_conf,
                                   d_verdict, (int)C, d_selected, d_counts, d_workspace, stream);
+}
+
+epic_status epic_commit_fallback(epic_ctx* c, const int32_t* d_seqs, int32_t B, int32_t n,
+                                 const int32_t* d_cand_seq, const int32_t* d_cand_pos, const int32_t* d_cand_tok,
+                                 const float* d_conf, const uint8_t* d_verdict, const uint8_t* d_selected,
+                                 const int32_t* d_num_commit, int32_t C, uint8_t* d_accepted, void* d_workspace,
+                                 size_t workspace_bytes, hipStream_t stream) {
+  epic_status s =
+      check_batch(c, d_seqs, B, n, d_cand_seq, d_cand_pos, d_cand_tok, C, d_accepted, d_workspace, workspace_bytes);
+  if (s != EPIC_OK || C == 0 || B == 0) return s;
+  if (!d_conf || !d_verdict || !d_selected || !d_num_commit) return EPIC_ERR_NULL;
+  return dispatch_w<FallbackLaunch>(c->H.W, c, d_seqs, (int)B, (int)n, d_cand_seq, d_cand_pos, d_cand_tok, d_conf,
+                                    d_verdict, d_selected, d_num_commit, (int)C, d_accepted, d_workspace, stream);
 }
 
 epic_status epic_ctx_device_error(epic_ctx* c, hipStream_t stream, uint32_t* flags) {

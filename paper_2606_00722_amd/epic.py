@@ -24,6 +24,7 @@ DEV_BAD_CANDIDATE, DEV_CAPACITY, DEV_BAD_SELECT = 1, 2, 4
 
 FUNCTIONS = ["epic_ctx_create", "epic_ctx_destroy", "epic_workspace_bytes", "epic_gap_classes", "epic_item_words",
              "epic_lexmemo_build", "epic_memo_export", "epic_validate_batch", "epic_select_compatible",
+             "epic_commit_fallback",
              "epic_ctx_device_error", "epic_ctx_work_counters", "epic_status_string"]
 
 
@@ -75,6 +76,8 @@ def lib() -> ctypes.CDLL:
         L.epic_validate_batch.restype = ctypes.c_int
         L.epic_select_compatible.argtypes = [P, P, i32, i32, P, P, P, P, P, i32, P, P, P, sz, P]
         L.epic_select_compatible.restype = ctypes.c_int
+        L.epic_commit_fallback.argtypes = [P, P, i32, i32, P, P, P, P, P, P, P, i32, P, P, sz, P]
+        L.epic_commit_fallback.restype = ctypes.c_int
         L.epic_ctx_device_error.argtypes = [P, P, ctypes.POINTER(ctypes.c_uint32)]
         L.epic_ctx_device_error.restype = ctypes.c_int
         L.epic_ctx_work_counters.argtypes = [P, P, P]
@@ -181,6 +184,14 @@ class Context:
         _check("epic_select_compatible", lib().epic_select_compatible(
             self._h, _ptr(seqs), B, n, _ptr(cand_seq), _ptr(cand_pos), _ptr(cand_tok), _ptr(conf), _ptr(verdict),
             int(cand_seq.numel()), _ptr(selected), _ptr(counts), wp, wb, _stream(stream)))
+
+    def fallback(self, seqs, cand_seq, cand_pos, cand_tok, conf, verdict, selected, num_commit, accepted, workspace,
+                 stream=None):
+        B, n = int(seqs.shape[0]), int(seqs.shape[1])
+        wp, wb = self._ws(workspace)
+        _check("epic_commit_fallback", lib().epic_commit_fallback(
+            self._h, _ptr(seqs), B, n, _ptr(cand_seq), _ptr(cand_pos), _ptr(cand_tok), _ptr(conf), _ptr(verdict),
+            _ptr(selected), _ptr(num_commit), int(cand_seq.numel()), _ptr(accepted), wp, wb, _stream(stream)))
 
     def work_counters(self, stream=None) -> np.ndarray:
         """int64[6]: walks, chart entries written, memo entries read, graph nodes,

@@ -182,6 +182,41 @@ def test_padded_grammar_item_widths(preset, words, gpu_mod, oracle_lib):
     assert np.array_equal(gs, ws) and gc == wc
 
 
+@pytest.mark.parametrize("batch", ["alg4", "empty"])
+@pytest.mark.parametrize("preset,B", [(1, None), (2, None), (3, 6), (4, 1)])
+def test_commit_fallback_matches_oracle(preset, B, batch, gpu_mod, oracle_lib):
+    """The sequential fallback after the relaxed batch, with the oracle's
+    verdicts as input and a seeded commit budget per sequence; the batch is
+    Alg. 4's selection, or empty (the case where the loop decides every
+    commit, accepting and rejecting candidates against the updated x).  The
+    candidates the device commits equal the oracle's, which checks every
+    candidate it reaches (the device walks verdict-1 ones only)."""
+    import torch
+
+    inst = W.make_instance(preset, 42, B=B)
+    pr = W.propose(inst)
+    p = oracle_lib.problem_from(inst.lang, inst.vocab)
+    v = oracle_lib.validate_batch(p, inst.seqs, pr.seq, pr.pos, pr.tok, NTH)
+    if batch == "alg4":
+        sel, _, st = oracle_lib.select(p, inst.seqs, pr.seq, pr.pos, pr.tok, pr.conf, v, NTH)
+        assert st == 0
+    else:
+        sel = np.zeros(pr.C, np.uint8)
+    rng = np.random.default_rng(100 + preset)
+    nc = rng.integers(1, 6 if preset == 4 else inst.cfg["props"] + 2, size=inst.B).astype(np.int32)
+    want, st = oracle_lib.fallback(p, inst.seqs, pr.seq, pr.pos, pr.tok, pr.conf, v, sel, nc)
+    assert st == 0
+    if batch == "empty":
+        assert want.sum() > 0
+    g = gpu_mod.Gpu(W.arrays(inst.lang, inst.vocab), inst.B, inst.n, max(pr.C, 64))
+    acc = torch.full((pr.C,), 7, dtype=torch.uint8, device=g.dev)
+    g.ctx.fallback(g.t(inst.seqs), g.t(pr.seq), g.t(pr.pos), g.t(pr.tok), g.t(pr.conf, torch.float32),
+                   g.t(v, torch.uint8), g.t(sel, torch.uint8), g.t(nc), acc, g.ws)
+    torch.cuda.synchronize()
+    assert g.errors() == 0
+    assert np.array_equal(acc.cpu().numpy(), want)
+
+
 @pytest.mark.parametrize("name,extra", [("tiny_paren", ["((", "))", "()"]), ("tiny_expr", ["a+", "(a", "a)", " a"]),
                                         ("tiny_kw", ["if", "(x", "x)", " i"]), ("tiny_ab", ["ab", "ba", "cc"]),
                                         ("arith", ["a+", "1*", "(a", " 1"])])

@@ -1,0 +1,56 @@
+"""Pins of the oracle's sequential fallback (the loop after the relaxed batch
+in EPIC decoding): it commits only what the exact check justifies, in
+confidence order, and no more than the step's budget."""
+import numpy as np
+
+from paper_2606_00722_amd import workloads as W
+
+
+def _step(oracle_lib, preset, seed=42):
+    inst = W.make_instance(preset, seed)
+    pr = W.propose(inst)
+    p = oracle_lib.problem_from(inst.lang, inst.vocab)
+    v = oracle_lib.validate_batch(p, inst.seqs, pr.seq, pr.pos, pr.tok, 4)
+    return inst, pr, p, v
+
+
+def test_budget_met_by_the_batch_commits_nothing(oracle_lib):
+    inst, pr, p, v = _step(oracle_lib, 1)
+    sel, _, st = oracle_lib.select(p, inst.seqs, pr.seq, pr.pos, pr.tok, pr.conf, v)
+    assert st == 0
+    nb = np.array([int(sel[pr.seq == b].sum()) for b in range(inst.B)])
+    acc, st = oracle_lib.fallback(p, inst.seqs, pr.seq, pr.pos, pr.tok, pr.conf, v, sel, nb)
+    assert st == 0 and acc.sum() == 0
+
+
+def test_first_commit_is_the_most_confident_valid_candidate(oracle_lib):
+    inst, pr, p, v = _step(oracle_lib, 1)
+    none = np.zeros(len(pr.seq), np.uint8)
+    acc, st = oracle_lib.fallback(p, inst.seqs, pr.seq, pr.pos, pr.tok, pr.conf, v, none, np.ones(inst.B, np.int64))
+    assert st == 0
+    for b in range(inst.B):
+        mine = np.flatnonzero(pr.seq == b)
+        ok = [c for c in mine if v[c] == 1]
+        want = min(ok, key=lambda c: (-float(pr.conf[c]), c)) if ok else None
+        got = np.flatnonzero(acc[mine])
+        assert (len(got) == 0) if want is None else (list(mine[got]) == [want])
+
+
+def test_commits_are_valid_within_budget_and_never_invalid_candidates(oracle_lib):
+    for preset in (1, 2):
+        inst, pr, p, v = _step(oracle_lib, preset)
+        sel, _, st = oracle_lib.select(p, inst.seqs, pr.seq, pr.pos, pr.tok, pr.conf, v)
+        assert st == 0
+        rng = np.random.default_rng(preset)
+        nc = rng.integers(0, inst.cfg["props"] + 2, size=inst.B)
+        acc, st = oracle_lib.fallback(p, inst.seqs, pr.seq, pr.pos, pr.tok, pr.conf, v, sel, nc)
+        assert st == 0
+        assert not np.any(acc & (v != 1)) and not np.any(acc & sel)
+        for b in range(inst.B):
+            mine = pr.seq == b
+            assert acc[mine].sum() <= max(0, nc[b] - sel[mine].sum())
+            x = inst.seqs[b].copy()
+            for c in np.flatnonzero(mine & ((sel == 1) | (acc == 1))):
+                x[pr.pos[c]] = pr.tok[c]
+            if sel[mine].sum() + acc[mine].sum():  # whatever was committed keeps x_b completable
+                assert oracle_lib.valid(p, x) == 1
