@@ -75,6 +75,7 @@ __device__ inline uint64_t grp_or64(uint64_t v) {
 // best on the C-like workloads of 256 and 1024 tokens.
 constexpr int kThreads = 512;
 constexpr int kThreadsWide = 1024;
+constexpr int kDoneChecks = 64;  // answered checks remembered per sequence by the selection
 // Alg. 4 runs several checks per sequence one after another; from this many
 // tokens on, each resumes from base walks of the sequence (prefix sharing).
 #ifndef EPIC_SHARE_SELECT_LEN
@@ -558,6 +559,12 @@ __global__ void __launch_bounds__(NT) select_kernel(DevTab tb, const int32_t* __
   __shared__ Frame stack[96];
   __shared__ int sp;
   __shared__ uint64_t ret_val, final_B;
+  // checks already answered for this sequence: Alg. 4 asks some again (after
+  // an exact check fails and a half passes, the next RelaxedSelect and
+  // ExactShrink repeat the cover and exact checks of the whole set)
+  __shared__ uint64_t done_msk[kDoneChecks];
+  __shared__ int done_val[kDoneChecks];  // result | (cover ? 2 : 0)
+  __shared__ int done_n, done_hit;
   const WgWork wk = slot_work(ws, blockIdx.x);
   stage_tables<W>(tb, L);
   int32_t* spec_state = spec;           // [B * kSpec]
@@ -583,6 +590,7 @@ __global__ void __launch_bounds__(NT) select_kernel(DevTab tb, const int32_t* __
       atomicOr(tb.dev_err, L.sel_bad == 2   ? (uint32_t)EPIC_DEV_CAPACITY
                            : L.sel_bad == 3 ? (uint32_t)EPIC_DEV_BAD_CANDIDATE
                                             : (uint32_t)EPIC_DEV_BAD_SELECT);
+    done_n = 0;
     sp = 0;
     stack[0] = Frame{kTop, 0, 0, m >= 64 ? ~0ull : ((1ull << m) - 1), 0};
     sp = 1;
@@ -679,7 +687,16 @@ __global__ void __launch_bounds__(NT) select_kernel(DevTab tb, const int32_t* __
       ++ncover;
     else
       ++nexact;
-    if (helpers) {
+    const int kind = req == kReqCover ? 2 : 0;
+    if (threadIdx.x == 0) {
+      int hit = -1;
+      for (int k = 0; k < done_n; ++k)
+        if (done_msk[k] == msk && (done_val[k] & 2) == kind) hit = done_val[k] & 1;
+      done_hit = hit;
+    }
+    __syncthreads();
+    r = done_hit;
+    if (r < 0 && helpers) {
       int q = -1;
       for (int qq = 1; qq < kSpec; ++qq)
         if (((qq & 1) != 0) == (req == kReqExact) && spec_mask(qq, L.sel_n) == msk) q = qq;
@@ -714,7 +731,14 @@ __global__ void __launch_bounds__(NT) select_kernel(DevTab tb, const int32_t* __
       failed = true;
       break;
     }
-    if (threadIdx.x == 0) L.sel_res = r;
+    if (threadIdx.x == 0) {
+      L.sel_res = r;
+      if (done_hit < 0 && done_n < kDoneChecks) {
+        done_msk[done_n] = msk;
+        done_val[done_n] = r | (req == kReqCover ? 2 : 0);
+        ++done_n;
+      }
+    }
     __syncthreads();
   }
   if (threadIdx.x == 0) {
