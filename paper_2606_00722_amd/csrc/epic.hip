@@ -527,17 +527,19 @@ EPIC_INLINE int select_walk(const DevTab& tb, Lds<W>& L, const WgWork& wk, const
 // publish each result with a state word (0 not started, 1 running, 2 done,
 // 3 not applicable).  The selection takes a result that is done, waits for
 // one that is running (its helper is resident and finishes on its own), and
-// otherwise walks the check itself.  Check r: r even = relaxed (cover),
-// odd = exact; r < 2 on all sorted candidates, r >= 2 on their
-// high-confidence half (the first ceil(m/2)).
-constexpr int kSpec = 4;
+// otherwise walks the check itself.  Checks, on prefixes of the m candidates
+// sorted by confidence (h = ceil(m/2), the high-confidence half): r = 1 exact
+// on all; 2 relaxed (cover) on h; 3 exact on h; then the next exact checks of
+// ExactShrink's search when the exact check on all fails: 4 on
+// h + ceil((m-h)/2) (the half passed), 5 on ceil(h/2) (it failed).  A
+// launch runs as many of them per sequence as the CUs hold.
+constexpr int kSpec = 6;  // state slots per sequence: slot 0 unused, checks 1..5
 constexpr long long kSpecWaitCycles = 4ll << 30;  // give up waiting on a helper after this many clocks
+__device__ inline bool spec_exact(int r) { return r != 2; }
 __device__ inline uint64_t spec_mask(int r, int m) {
-  const uint64_t all = m >= 64 ? ~0ull : ((1ull << m) - 1);
-  if (r < 2) return all;
-  uint64_t lo, hi;
-  split_halves(all, lo, hi);
-  return lo;
+  const int h = (m + 1) / 2;
+  const int len = r < 2 ? m : r == 4 ? h + (m - h + 1) / 2 : r == 5 ? (h + 1) / 2 : h;
+  return len >= 64 ? ~0ull : ((1ull << len) - 1);
 }
 
 template <int W>
@@ -574,9 +576,10 @@ __global__ void __launch_bounds__(NT) select_kernel(DevTab tb, const int32_t* __
   // through the one call site of each check type below.
   const bool helper = (int)blockIdx.x >= B;
   const int hi = helper ? (int)blockIdx.x - B : 0;
-  const int b = helper ? hi / (kSpec - 1) : (int)blockIdx.x;
-  const int hr = 1 + hi % (kSpec - 1);
-  const bool helpers = (int)gridDim.x > B;
+  const int nh = (int)gridDim.x / B - 1;  // helpers per sequence
+  const int b = helper ? hi / nh : (int)blockIdx.x;
+  const int hr = helper ? 1 + hi % nh : 0;
+  const bool helpers = nh > 0;
   const int bad = select_setup<W>(tb, L, seqs, n, cseq, cpos, ctok, conf, verdict, C, b, helper ? nullptr : selected);
   if (helper) {
     if (bad || __popcll(spec_mask(hr, L.sel_n)) < 2) {  // Alg. 4 checks no subset of one candidate
@@ -606,7 +609,7 @@ __global__ void __launch_bounds__(NT) select_kernel(DevTab tb, const int32_t* __
     uint64_t msk;
     int r = -1;
     if (helper) {
-      req = (hr & 1) ? kReqExact : kReqCover;
+      req = spec_exact(hr) ? kReqExact : kReqCover;
       msk = spec_mask(hr, L.sel_n);
     } else {
     if (threadIdx.x == 0) {
@@ -698,8 +701,8 @@ __global__ void __launch_bounds__(NT) select_kernel(DevTab tb, const int32_t* __
     r = done_hit;
     if (r < 0 && helpers) {
       int q = -1;
-      for (int qq = 1; qq < kSpec; ++qq)
-        if (((qq & 1) != 0) == (req == kReqExact) && spec_mask(qq, L.sel_n) == msk) q = qq;
+      for (int qq = 1; qq <= nh; ++qq)
+        if (spec_exact(qq) == (req == kReqExact) && spec_mask(qq, L.sel_n) == msk) q = qq;
       if (q > 0 && threadIdx.x == 0) {
         int res = -1;
         const long long t_start = (long long)clock64();
@@ -998,9 +1001,11 @@ epic_status SelectLaunch<W>::run(epic_ctx* c, const int32_t* seqs, int B, int n,
                                  const int32_t* cp, const int32_t* ct, const float* conf, const uint8_t* verdict,
                                  int C, uint8_t* sel, int64_t* counts, void* ws, hipStream_t stream) {
   int32_t* spec = (int32_t*)((char*)ws + c->off_spec);
-  // B selection workgroups, then (kSpec - 1) helpers per sequence when the
-  // workspace has chart storage for all of them
-  const int grid = B * kSpec <= c->nslot ? B * kSpec : B;
+  // B selection workgroups, then up to kSpec - 1 helpers per sequence, as
+  // many as leave every workgroup a CU, when the workspace has chart storage
+  // for all of them
+  const int nh = std::min(kSpec - 1, c->num_cus / B - 1);
+  const int grid = nh >= 1 && B * (nh + 1) <= c->nslot ? B * (nh + 1) : B;
   const WsArgs wa = ws_args(c, ws);
   // long sequences: Alg. 4's checks resume from base walks of both graphs
   const int share = n >= kShareSelectLen && B <= c->base_slots;
