@@ -217,6 +217,47 @@ def test_commit_fallback_matches_oracle(preset, B, batch, gpu_mod, oracle_lib):
     assert np.array_equal(acc.cpu().numpy(), want)
 
 
+def test_commit_fallback_edge_cases(gpu_mod, oracle_lib):
+    """Zero budget, a budget above the candidate count, a repeated position
+    among one sequence's valid candidates (that sequence commits nothing and
+    sets EPIC_DEV_BAD_SELECT, the others match the oracle), and C = 0."""
+    import torch
+
+    from paper_2606_00722_amd import epic
+
+    inst = W.make_instance(1, 42)
+    pr = W.propose(inst)
+    p = oracle_lib.problem_from(inst.lang, inst.vocab)
+    v = oracle_lib.validate_batch(p, inst.seqs, pr.seq, pr.pos, pr.tok, NTH)
+    g = gpu_mod.Gpu(W.arrays(inst.lang, inst.vocab), inst.B, inst.n, max(pr.C, 64))
+    none = np.zeros(pr.C, np.uint8)
+
+    def run(pos, nc, C=None):
+        C = pr.C if C is None else C
+        acc = torch.full((max(C, 1),), 7, dtype=torch.uint8, device=g.dev)
+        g.ctx.fallback(g.t(inst.seqs), g.t(pr.seq[:C]), g.t(pos[:C]), g.t(pr.tok[:C]),
+                       g.t(pr.conf[:C], torch.float32), g.t(v[:C], torch.uint8), g.t(none[:C], torch.uint8),
+                       g.t(nc), acc[:C], g.ws)
+        torch.cuda.synchronize()
+        return acc[:C].cpu().numpy()
+
+    assert not run(pr.pos, np.zeros(inst.B, np.int32)).any() and g.errors() == 0
+    big = np.full(inst.B, 64, np.int32)
+    want, st = oracle_lib.fallback(p, inst.seqs, pr.seq, pr.pos, pr.tok, pr.conf, v, none, big)
+    assert st == 0 and want.sum() > 0
+    assert np.array_equal(run(pr.pos, big), want) and g.errors() == 0
+    b0 = next(b for b in range(inst.B) if ((pr.seq == b) & (v == 1)).sum() >= 2)
+    c1, c2 = np.flatnonzero((pr.seq == b0) & (v == 1))[:2]
+    pos2 = pr.pos.copy()
+    pos2[c2] = pos2[c1]
+    want2, st2 = oracle_lib.fallback(p, inst.seqs, pr.seq, pos2, pr.tok, pr.conf, v, none, big)
+    assert st2 == -4 and not want2[pr.seq == b0].any()
+    got2 = run(pos2, big)
+    assert np.array_equal(got2, want2)
+    assert g.errors() & epic.DEV_BAD_SELECT
+    assert run(pr.pos, big, C=0).size == 0 and g.errors() == 0
+
+
 @pytest.mark.parametrize("name,extra", [("tiny_paren", ["((", "))", "()"]), ("tiny_expr", ["a+", "(a", "a)", " a"]),
                                         ("tiny_kw", ["if", "(x", "x)", " i"]), ("tiny_ab", ["ab", "ba", "cc"]),
                                         ("arith", ["a+", "1*", "(a", " 1"])])
