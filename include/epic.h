@@ -45,7 +45,7 @@ typedef enum {
   EPIC_ERR_VOCAB = -6,       /* token empty or longer than 8 bytes */
   EPIC_ERR_HIP = -7,         /* a HIP runtime call failed */
   EPIC_ERR_STATE = -8,       /* memo not built yet */
-  EPIC_ERR_UNSUPPORTED = -9  /* outside the sizes this build supports (see below) */
+  EPIC_ERR_UNSUPPORTED = -9  /* outside the sizes the library supports (see below) */
 } epic_status;
 
 /* Device-side sticky error bits, read by epic_ctx_device_error(). */

@@ -4,7 +4,7 @@ The paper decodes with diffusion LMs on HumanEval-X C++, a JSON-schema
 benchmark and a SMILES benchmark (App. E.2).  Neither models nor datasets are
 used here: these generators stand in for them with seeded inputs of the same
 kind and shape (vocabularies, partially masked answers, proposals and
-confidences).  Five named presets follow the workload table of this build:
+confidences).  Five named presets:
 
 =====  ========  ======  ====  ========  ==================  ==========  =====
 preset language  vocab   Lmax  B x n     masking             props/seq   steps
