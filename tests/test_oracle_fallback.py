@@ -54,3 +54,28 @@ def test_commits_are_valid_within_budget_and_never_invalid_candidates(oracle_lib
                 x[pr.pos[c]] = pr.tok[c]
             if sel[mine].sum() + acc[mine].sum():  # whatever was committed keeps x_b completable
                 assert oracle_lib.valid(p, x) == 1
+
+
+def test_invalid_candidates_stay_invalid_after_commits(oracle_lib):
+    """The reading the device's fallback relies on: filling masked positions
+    only shrinks the character language of x, so a candidate invalid on x is
+    invalid on x with Alg. 4's batch committed (checked for every verdict-0
+    candidate of two workloads)."""
+    checked = 0
+    for preset in (1, 2):
+        inst, pr, p, v = _step(oracle_lib, preset)
+        sel, _, st = oracle_lib.select(p, inst.seqs, pr.seq, pr.pos, pr.tok, pr.conf, v)
+        assert st == 0
+        for b in range(inst.B):
+            mine = pr.seq == b
+            x = inst.seqs[b].copy()
+            for c in np.flatnonzero(mine & (sel == 1)):
+                x[pr.pos[c]] = pr.tok[c]
+            for c in np.flatnonzero(mine & (v == 0)):
+                if x[pr.pos[c]] != -1:
+                    continue
+                y = x.copy()
+                y[pr.pos[c]] = pr.tok[c]
+                assert oracle_lib.valid(p, y) == 0
+                checked += 1
+    assert checked > 10
