@@ -204,17 +204,18 @@ def select(p: Problem, seqs: np.ndarray, seq, pos, tok, conf, verdict, nthreads:
     return out[:C], (int(stats[0]), int(stats[1])), int(r)
 
 
-def fallback(p: Problem, seqs: np.ndarray, seq, pos, tok, conf, verdict, selected, num_commit):
-    """The sequential fallback after the relaxed batch in EPIC decoding (App. E,
-    the decoding algorithm and the paragraph after it), taken step by step:
+def fallback(p: Problem, seqs: np.ndarray, seq, pos, tok, conf, verdict, selected, num_commit, nthreads: int = 1):
+    """The sequential fallback after the relaxed batch in EPIC decoding (App. C.1,
+    Alg. 1 and the paragraph after it), taken step by step:
     per sequence b, commit the selected set B to x_b, then walk the remaining
     candidates of b by descending confidence (ties to the lower index) and
     commit each whose exact check Valid(x_b + c) holds on the current x_b, until
     num_commit[b] - |B| more are committed or the candidates run out.  Every
     candidate is checked whatever its verdict; one whose position is no longer
-    masked cannot be applied and is passed over.  Input rules as in `select`: a
+    masked cannot be applied and is passed over.  Input rule as in `select`: a
     sequence whose verdict-1 candidates repeat a position or carry a NaN
-    confidence, or number more than 64, commits nothing (status -4 or -2).
+    confidence commits nothing (status -4).  There is no limit on the number
+    of candidates (Alg. 1 has none).  `nthreads` runs sequences concurrently.
     Returns (accepted uint8[C], status)."""
     s = np.ascontiguousarray(seqs, dtype=np.int32)
     cs, cp, ct = _cands(seq, pos, tok)
@@ -224,16 +225,12 @@ def fallback(p: Problem, seqs: np.ndarray, seq, pos, tok, conf, verdict, selecte
     nc = np.asarray(num_commit, dtype=np.int64)
     C = int(cs.size)
     acc = np.zeros(C, dtype=np.uint8)
-    status = 0
-    for b in range(s.shape[0]):
+
+    def one(b: int) -> int:  # sequences are independent: one loop each
         mine = [c for c in range(C) if cs[c] == b]
         v1 = [c for c in mine if vd[c] == 1]
         if any(np.isnan(cf[c]) for c in v1) or len({int(cp[c]) for c in v1}) < len(v1):
-            status = -4
-            continue
-        if len(v1) > 64:
-            status = -2
-            continue
+            return -4
         x = s[b].copy()
         committed = [c for c in mine if sl[c]]
         for c in committed:
@@ -252,4 +249,13 @@ def fallback(p: Problem, seqs: np.ndarray, seq, pos, tok, conf, verdict, selecte
                 x = y
                 acc[c] = 1
                 need -= 1
-    return acc, status
+        return 0
+
+    if nthreads > 1 and s.shape[0] > 1:
+        from concurrent.futures import ThreadPoolExecutor
+
+        with ThreadPoolExecutor(nthreads) as ex:  # the oracle's C calls release the GIL
+            sts = list(ex.map(one, range(s.shape[0])))
+    else:
+        sts = [one(b) for b in range(s.shape[0])]
+    return acc, min(sts, default=0)

@@ -79,3 +79,24 @@ def test_invalid_candidates_stay_invalid_after_commits(oracle_lib):
                 assert oracle_lib.valid(p, y) == 0
                 checked += 1
     assert checked > 10
+
+
+def test_no_limit_on_the_number_of_candidates(oracle_lib):
+    """Alg. 1's loop has no cap on the candidates it walks: one sequence with
+    every masked position proposed with its hidden token (about a hundred
+    candidates, each valid, and jointly valid since the hidden answer fills
+    them) commits exactly the budget, in confidence order."""
+    inst = W.make_instance(1, 42, B=1, n=200)
+    masked = np.flatnonzero(inst.seqs[0] == W.MASK).astype(np.int32)
+    assert len(masked) > 64
+    C = len(masked)
+    seq = np.zeros(C, np.int32)
+    tok = inst.hidden[0, masked].astype(np.int32)
+    conf = np.random.default_rng(7).random(C, dtype=np.float32)
+    p = oracle_lib.problem_from(inst.lang, inst.vocab)
+    v = np.ones(C, np.uint8)
+    budget = 70
+    acc, st = oracle_lib.fallback(p, inst.seqs, seq, masked, tok, conf, v, np.zeros(C, np.uint8), [budget])
+    assert st == 0 and int(acc.sum()) == budget
+    order = sorted(range(C), key=lambda c: (-float(conf[c]), c))
+    assert set(np.flatnonzero(acc).tolist()) == set(order[:budget])
