@@ -39,9 +39,10 @@ def source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def pmc_traffic(kernel: str, preset: int):
-    """HBM bytes per launch from profiles/<kernel>_preset<p>_pmc.json if it
-    matches the current sources."""
+def pmc_summary(kernel: str, preset: int):
+    """The committed rocprofv3 counter summary of a kernel kind on a workload
+    (profiles/<kernel>_preset<p>_pmc.json: HBM bytes per launch, LDS and VALU
+    figures) if it was taken on the current kernel sources, else None."""
     path = os.path.join(PROFILES, f"{kernel}_preset{preset}_pmc.json")
     if not os.path.exists(path):
         return None
@@ -49,7 +50,7 @@ def pmc_traffic(kernel: str, preset: int):
         d = json.load(f)
     if d.get("source_hash") != source_hash():
         return None
-    return d.get("hbm_bytes_per_launch")
+    return d
 
 
 def copy_calibration(mib: int) -> int:
@@ -65,14 +66,83 @@ def copy_calibration(mib: int) -> int:
     return 0
 
 
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(inst, traj, budget_s: float) -> dict:
+    """The oracle, untuned, on the host cores: validity checks of the first
+    step's candidates (cycled) on one thread and on all threads of the CPU
+    share, Alg. 4 selections of its sequences the same way, and one memo
+    build, within about `budget_s` seconds in all."""
+    import numpy as np
+
+    import oracle
+
+    p = oracle.problem_from(inst.lang, inst.vocab)
+    host_cpus = len(os.sched_getaffinity(0))
+    nall = max(1, min(16, host_cpus))  # one GPU's share of the host
+    x0, pr0 = traj[0]["host"]
+    v0 = traj[0]["ref"][0]
+
+    def checks(nth: int, secs: float):
+        done, spent = 0, 0.0
+        while spent < secs and done < 50 * pr0.C:
+            idx = (done + np.arange(max(1, 2 * nth))) % pr0.C
+            ts = time.perf_counter()
+            oracle.validate_batch(p, x0, pr0.seq[idx], pr0.pos[idx], pr0.tok[idx], nth)
+            spent += time.perf_counter() - ts
+            done += len(idx)
+        return done, spent
+
+    def selections(nth: int, secs: float):
+        done, spent, b = 0, 0.0, 0
+        while spent < secs and done < 4 * inst.B:
+            seqs = [(b + i) % inst.B for i in range(max(1, nth))]
+            b += len(seqs)
+            idx = np.flatnonzero(np.isin(pr0.seq, seqs))
+            ts = time.perf_counter()
+            oracle.select(p, x0, pr0.seq[idx], pr0.pos[idx], pr0.tok[idx], pr0.conf[idx], v0[idx], nth)
+            spent += time.perf_counter() - ts
+            done += len(seqs)
+        return done, spent
+
+    ts = time.perf_counter()
+    oracle.memo(p)
+    memo_s = time.perf_counter() - ts
+    share = max(0.0, budget_s - memo_s) / 4
+    c1, s1 = checks(1, share)
+    cn, sn = checks(nall, share)
+    q1, t1 = selections(1, share)
+    qn, tn = selections(nall, share)
+    return {"value": round(cn / sn, 3), "unit": "checks/s", "cores": nall, "kind": "oracle",
+            "sample": f"{cn} validity checks of the first step of the same workload (its {pr0.C} candidates "
+                      f"cycled), {nall} threads, {sn:.1f} s",
+            "one_core": {"value": round(c1 / s1, 3), "unit": "checks/s", "sample": f"{c1} checks, {s1:.1f} s"},
+            "select": {"unit": "sequences/s", "one_core": round(q1 / t1, 4),
+                       "all_cores": round(qn / tn, 4),
+                       "sample": f"Alg. 4 on {q1} and {qn} sequences of the first step, {t1:.1f} s and {tn:.1f} s"},
+            "memo_build_s": round(memo_s, 3), "cpu_model": cpu_model(), "host_cpus": host_cpus,
+            "threads_note": "all cores = the host CPUs this process may use, at most 16 (one GPU's share)"}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=40)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--preset", type=int, default=2, help="workload preset 1..5 (default 2: JSON-like)")
+    ap.add_argument("--preset", type=int, default=5,
+                    help="workload preset 1..5 (default 5: C-like, 64 x 1024 tokens, the largest configuration)")
     ap.add_argument("--seed", type=int, default=42)
-    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="time budget of the oracle baseline")
+    ap.add_argument("--cpu-seconds", type=float, default=24.0,
+                    help="time budget of the oracle baseline (all legs together)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="run only a plain device copy of MIB MiB, 5 launches (the reference kernel that "
@@ -146,7 +216,8 @@ def main() -> int:
     for k in range(args.warmup):
         step(traj[k % len(traj)])
     torch.cuda.synchronize()
-    ctx.work_counters()  # clear
+    ctx.set_timing(True)  # HIP events around every kernel, on its stream
+    ctx.kernel_stats()  # clear
     log("timing")
     checks = 0
     t0 = time.perf_counter()
@@ -156,7 +227,8 @@ def main() -> int:
         checks += d["C"]
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
-    work_timed = ctx.work_counters()
+    kstats = ctx.kernel_stats()
+    ctx.set_timing(False)
     # outputs of the timed steps equal the generation run (deterministic path)
     for d in traj:
         if not (np.array_equal(d["verdict"].cpu().numpy(), d["ref"][0])
@@ -167,61 +239,79 @@ def main() -> int:
         print("device error flags set", file=sys.stderr)
         return 1
 
+    # the sequential fallback after the batch (Alg. 1), timed on its own over
+    # the same steps: per sequence a budget of all its proposals, so that the
+    # loop checks every valid candidate the batch left
+    fb_ms, fb_commits = [], 0
+    for d in traj:
+        nc = np.bincount(d["host"][1].seq, minlength=inst.B).astype(np.int32)
+        d["nc"] = t(nc)
+        d["accepted"] = torch.zeros(d["C"], dtype=torch.uint8, device=dev)
+    for d in traj[:2]:  # warm
+        ctx.fallback(d["seqs"], d["cs"], d["cp"], d["ct"], d["cf"], d["verdict"], d["selected"], d["nc"],
+                     d["accepted"], ws)
+    torch.cuda.synchronize()
+    for k in range(args.steps):
+        d = traj[k % len(traj)]
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        ctx.fallback(d["seqs"], d["cs"], d["cp"], d["ct"], d["cf"], d["verdict"], d["selected"], d["nc"],
+                     d["accepted"], ws)
+        e1.record()
+        fb_ms.append((e0, e1))
+    torch.cuda.synchronize()
+    for k in range(args.steps):
+        fb_commits += int(traj[k % len(traj)]["accepted"].sum().item())
+    if ctx.device_error() != 0:
+        print("device error flags set by the fallback", file=sys.stderr)
+        return 1
+
     ms = {"lexmemo": [], "validate": [], "select": []}
     for e in ev:
         ms["lexmemo"].append(e[0].elapsed_time(e[1]))
         ms["validate"].append(e[1].elapsed_time(e[2]))
         ms["select"].append(e[2].elapsed_time(e[3]))
-    avg = {k: float(np.mean(v)) for k, v in ms.items()}
+    phase = {k: float(np.mean(v)) for k, v in ms.items()}
+    fallback_ms = float(np.mean([a.elapsed_time(b) for a, b in fb_ms]))
 
-    # algorithmic bytes per launch, from one counted pass per kernel
+    # algorithmic bytes of the walks of one kernel kind, from its work
+    # counters over the timed steps: chart entries written (4W B of items,
+    # 8 B expected nonterminals, 8 B expected terminals, 4 B origin), memo
+    # entries read (16 B), chart entries pulled by row tasks (origin, summary
+    # and items: 12 + 4W B), one sequence row per walk (4n B)
     Wd = ctx.item_words
 
-    def walk_bytes(c, launches):
-        # chart entries written (4W B of items, 8 B expected nonterminals, 8 B
-        # expected terminals, 4 B origin), memo entries read (16 B), chart
-        # entries pulled by row tasks (origin, summary and items: 12 + 4W B),
-        # one sequence row per walk (4n B)
-        return (c[1] * (4 * Wd + 20) + c[2] * 16 + c[4] * (12 + 4 * Wd) + c[0] * 4 * inst.n) / launches
+    def walk_bytes(c):
+        return float(c[1] * (4 * Wd + 20) + c[2] * 16 + c[4] * (12 + 4 * Wd) + c[0] * 4 * inst.n)
 
-    for d in traj:
-        ctx.validate(d["seqs"], d["cs"], d["cp"], d["ct"], d["verdict"], ws)
-    cv = ctx.work_counters()
-    for d in traj:
-        ctx.select(d["seqs"], d["cs"], d["cp"], d["ct"], d["cf"], d["verdict"], d["selected"], ws)
-    cs = ctx.work_counters()
     V, Q = ctx.vocab_size, ctx.num_states
-    bytes_per = {
-        "lexmemo": 16.0 * V * Q + 4.0 * (V + 1) + float(arr.voffs[-1]) + 512.0 * Q,
-        "validate": walk_bytes(cv, len(traj)),
-        "select": walk_bytes(cs, len(traj)),
-    }
-    dom = max(avg, key=lambda k: avg[k])
-    achieved = bytes_per[dom] / (avg[dom] * 1e-3) / 1e9
-    traffic = pmc_traffic(dom, args.preset)
+    kern = {}
+    for k, st in kstats.items():
+        if st["launches"] == 0:
+            continue
+        by = (16.0 * V * Q + 4.0 * (V + 1) + float(arr.voffs[-1]) + 512.0 * Q) * st["launches"] \
+            if k == "lexmemo" else walk_bytes(st["work"])
+        kern[k] = {"ms_per_launch": st["ms"] / st["launches"], "launches_per_step": st["launches"] / args.steps,
+                   "ms_per_step": st["ms"] / args.steps, "bytes": by, "launches": st["launches"],
+                   "walks_per_step": int(st["work"][0]) / args.steps}
+    dom = max(kern, key=lambda k: kern[k]["ms_per_step"])
+    kd = kern[dom]
+    bytes_per_launch = kd["bytes"] / kd["launches"]
+    achieved = bytes_per_launch / (kd["ms_per_launch"] * 1e-3) / 1e9
+    pmc = pmc_summary(dom, args.preset)
     roof = {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 3), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": round(achieved / HBM_PEAK_GBS, 6), "traffic": traffic,
-            "bytes_per_launch": round(bytes_per[dom], 1), "ms_per_launch": round(avg[dom], 4)}
+            "frac": round(achieved / HBM_PEAK_GBS, 6),
+            "traffic": pmc.get("hbm_bytes_per_launch") if pmc else None,
+            "bytes_per_launch": round(bytes_per_launch, 1), "ms_per_launch": round(kd["ms_per_launch"], 4)}
+    if pmc:
+        for key in ("lds", "valu", "occupancy"):
+            if key in pmc:
+                roof[key] = pmc[key]
 
     cpu = None
     if not args.no_cpu_baseline:
         log("cpu baseline")
-        import oracle
-
-        p = oracle.problem_from(inst.lang, inst.vocab)
-        nth = min(16, os.cpu_count() or 1)
-        done, spent = 0, 0.0
-        x0, pr0 = traj[0]["host"]
-        order = np.arange(pr0.C)
-        while spent < args.cpu_seconds and done < 50 * pr0.C:
-            idx = order[(done + np.arange(nth)) % pr0.C]
-            ts = time.perf_counter()
-            oracle.validate_batch(p, x0, pr0.seq[idx], pr0.pos[idx], pr0.tok[idx], nth)
-            spent += time.perf_counter() - ts
-            done += len(idx)
-        cpu = {"value": round(done / spent, 3), "unit": "checks/s", "cores": nth, "kind": "oracle",
-               "sample": f"{done} validity checks of step 1 of the same workload (candidates cycled), "
-                         f"{nth} threads, {spent:.1f} s"}
+        cpu = cpu_baseline(inst, traj, args.cpu_seconds)
 
     line = {
         "metric": METRIC, "value": round(checks / elapsed, 2), "unit": "checks/s", "n_gpus": 1,
@@ -230,8 +320,12 @@ def main() -> int:
         "config": {"workload": W.PRESET_NAMES[args.preset], "preset": args.preset, "batch": inst.B,
                    "seq_len": inst.n, "candidates_per_step": props_per_step, "steps_cycled": len(traj),
                    "seed": args.seed, "parallelism": "none (1 GPU)"},
-        "kernels_ms": {k: round(v, 4) for k, v in avg.items()},
-        "work_per_step": {"walks": int(work_timed[0] // args.steps), "chart_entries": int(work_timed[1] // args.steps)},
+        "phases_ms": {**{k: round(v, 4) for k, v in phase.items()}, "fallback": round(fallback_ms, 4)},
+        "kernels_ms": {k: {"ms_per_launch": round(v["ms_per_launch"], 4),
+                           "launches_per_step": round(v["launches_per_step"], 3),
+                           "walks_per_step": round(v["walks_per_step"], 1)} for k, v in kern.items()},
+        "fallback": {"ms_per_call": round(fallback_ms, 4), "commits_per_call": round(fb_commits / args.steps, 2),
+                     "budget": "per sequence, all of its proposals", "in_step": False},
         "roofline": roof,
         "cpu_baseline": cpu,
     }

@@ -105,15 +105,21 @@ epic_status epic_ctx_create(const epic_lexer_desc* lexer, const epic_grammar_des
 void epic_ctx_destroy(epic_ctx* ctx);
 
 /* Bytes of device workspace that epic_validate_batch,
- * epic_select_compatible and epic_commit_fallback need (the caller allocates it, 256-byte aligned).
+ * epic_select_compatible and epic_commit_fallback need (the caller allocates
+ * it, 256-byte aligned, and zeroes it once after allocating it).
  * Besides per-call scratch the workspace keeps, between calls, the recorded
  * walks of each sequence (its chart state at every masked run, tagged with the
  * context and the sequence walked).  A later call on the same context and
  * workspace resumes a sequence's walk at the last recorded masked run that
- * starts at or before the first token that changed; any other workspace
- * contents (fresh, zeroed, another context's) are detected by the tag and
- * walked from the start.  The caller must not modify the workspace between
- * calls; results do not depend on its contents, only the time taken does. */
+ * starts at or before the first token that changed.  Records of another
+ * context (other tables, another process, or a context since destroyed) fail
+ * the tag check and the sequence is walked from the start, as in a zeroed
+ * workspace.  The tag covers the record headers, not the chart storage they
+ * point into, so the caller must zero a newly allocated workspace (memory
+ * that held this context's earlier workspace could otherwise carry valid
+ * headers over overwritten charts) and must not modify it between calls;
+ * under these two rules results do not depend on its contents, only the time
+ * taken does. */
 size_t epic_workspace_bytes(const epic_ctx* ctx);
 
 /* Number of graph nodes one masked run contributes: the left-language
@@ -178,7 +184,7 @@ epic_status epic_select_compatible(epic_ctx* ctx, const int32_t* d_seqs, int32_t
                                    hipStream_t stream);
 
 /* The sequential fallback that follows the relaxed batch in EPIC decoding
- * (App. E, the decoding algorithm and the paragraph after it): per sequence b,
+ * (App. C.1: Alg. 1 and the paragraph after it): per sequence b,
  * with the selected set B (d_selected, as written by epic_select_compatible)
  * committed to x_b, the other candidates of b are taken by descending
  * confidence (float32, ties to the lower candidate index); each is committed
@@ -211,6 +217,21 @@ epic_status epic_ctx_device_error(epic_ctx* ctx, hipStream_t stream, uint32_t* f
  * completion and scan steps (summary and origin read), out[5] of those,
  * entries whose items were read. */
 epic_status epic_ctx_work_counters(epic_ctx* ctx, hipStream_t stream, int64_t* out);
+
+/* Diagnostics: per-kernel timing.  With enable != 0, every kernel the
+ * context launches from then on is bracketed by two HIP events recorded on the
+ * stream it is launched on (the events cost a few microseconds per launch).
+ * Off by default. */
+epic_status epic_ctx_set_timing(epic_ctx* ctx, int32_t enable);
+
+/* Diagnostics: synchronise `stream`, then read and clear, per kernel kind k
+ * (0 lexing memo, 1 base walks of prefix sharing, 2 candidate walks of
+ * validation, 3 selection with its helper workgroups, 4 sequential fallback,
+ * 5 speculation-state clear): ms[k] the summed event durations of its timed
+ * launches, launches[k] their number, work[k*6 .. k*6+5] the work counters of
+ * its walks (as epic_ctx_work_counters).  Host arrays of 6, 6 and 36
+ * elements. */
+epic_status epic_ctx_kernel_stats(epic_ctx* ctx, hipStream_t stream, double* ms, int64_t* launches, int64_t* work);
 
 const char* epic_status_string(epic_status s);
 

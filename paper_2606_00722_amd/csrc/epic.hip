@@ -19,6 +19,7 @@
 #include <cstdio>
 #include <cstring>
 #include <mutex>
+#include <random>
 #include <string>
 #include <vector>
 
@@ -760,7 +761,7 @@ __global__ void __launch_bounds__(NT) select_kernel(DevTab tb, const int32_t* __
 
 // ------------------------------------------------------------------ fallback
 // The sequential fallback that follows the relaxed batch in EPIC decoding
-// (the decoding algorithm of App. E, and the paragraph after it): with the
+// (Alg. 1 in App. C.1, and the paragraph after it): with the
 // selected set B committed, the remaining candidates of sequence b are taken
 // by descending confidence (ties to the lower candidate index) and each is
 // committed when x + (everything committed so far) + c is valid, until
@@ -825,6 +826,13 @@ __global__ void __launch_bounds__(NT) fallback_kernel(DevTab tb, const int32_t* 
 // ==================================================================== C ABI
 using namespace epic;
 
+// Kernel kinds for the diagnostics: each kind's walks add to a work-counter
+// set of its own, and with timing on each launch is bracketed by HIP events.
+enum : int { kKLexmemo = 0, kKBase, kKValidate, kKSelect, kKFallback, kKSpecClear, kKernelKinds };
+constexpr int kWorkCounters = 6;   // counters per set (see epic_ctx_work_counters)
+constexpr size_t kWorkOff = 64;    // byte offset of the counter sets in the error block
+constexpr size_t kErrBlock = 1024; // bytes of the error / counter block
+
 struct epic_ctx {
   HostTables H;
   int max_batch = 0, max_seq = 0, max_cands = 0;
@@ -842,6 +850,15 @@ struct epic_ctx {
   size_t off_snap = 0, snap_bytes = 0, off_spec = 0, off_bseq = 0;
   uint64_t tag = 0;  // owner tag of the base records this context writes
   bool cover_bases = false;  // the last base launch also walked the cover graphs
+  // diagnostics: per-kernel HIP-event timing (epic_ctx_set_timing)
+  bool timing = false;
+  struct Pending {
+    int kid;
+    hipEvent_t a, b;
+  };
+  std::vector<Pending> pending;
+  double kernel_ms[kKernelKinds] = {};
+  int64_t kernel_launches[kKernelKinds] = {};
 };
 
 namespace {
@@ -868,11 +885,31 @@ epic_status upload(epic_ctx* c) {
          o_enib = place(blob, H.expn_nib), o_pnib = place(blob, H.pred_nib), o_gcov = place(blob, H.gap_cover),
          o_lnib = place(blob, H.lhs_nib), o_snib = place(blob, H.sym_nib),
          o_vb = place(blob, H.vbytes), o_vo = place(blob, H.voffs);
+  {
+    // owner tag of the walk records this context writes: FNV-1a over every
+    // constant table (the memo is a function of them) and the workspace
+    // layout, mixed with a per-process random value and a per-context count,
+    // so that records of another context, another process or other tables
+    // never match
+    uint64_t h = 1469598103934665603ull;
+    auto mix = [&h](const void* p, size_t n) {
+      const unsigned char* b = (const unsigned char*)p;
+      for (size_t i = 0; i < n; ++i) h = (h ^ b[i]) * 1099511628211ull;
+    };
+    mix(blob.data(), blob.size());
+    const size_t layout[] = {c->slot_bytes, (size_t)c->maxn, (size_t)c->maxe, (size_t)c->nslot,
+                             (size_t)c->base_slots, (size_t)c->max_seq, c->snap_bytes, c->off_snap, c->off_bseq};
+    mix(layout, sizeof(layout));
+    static const uint64_t nonce = ((uint64_t)std::random_device{}() << 32) ^ std::random_device{}();
+    static std::atomic<uint64_t> counter{1};
+    c->tag = h ^ (nonce + 0x9E3779B97F4A7C15ull * counter.fetch_add(1));
+    if (c->tag == 0) c->tag = 1;  // a zeroed header never matches
+  }
   if (hipMalloc(&c->d_tables, blob.size()) != hipSuccess) return EPIC_ERR_HIP;
   if (hipMemcpy(c->d_tables, blob.data(), blob.size(), hipMemcpyHostToDevice) != hipSuccess) return EPIC_ERR_HIP;
   if (hipMalloc((void**)&c->d_memo, (size_t)H.V * H.Q * sizeof(uint4)) != hipSuccess) return EPIC_ERR_HIP;
-  if (hipMalloc((void**)&c->d_err, 256) != hipSuccess) return EPIC_ERR_HIP;
-  if (hipMemset(c->d_err, 0, 256) != hipSuccess) return EPIC_ERR_HIP;
+  if (hipMalloc((void**)&c->d_err, kErrBlock) != hipSuccess) return EPIC_ERR_HIP;
+  if (hipMemset(c->d_err, 0, kErrBlock) != hipSuccess) return EPIC_ERR_HIP;
   char* d = (char*)c->d_tables;
   DevTab& t = c->tab;
   t.Q = H.Q;
@@ -915,7 +952,7 @@ epic_status upload(epic_ctx* c) {
   t.voffs = (const int32_t*)(d + o_vo);
   t.memo = c->d_memo;
   t.dev_err = c->d_err;
-  t.work = (unsigned long long*)((char*)c->d_err + 64);
+  t.work = (unsigned long long*)((char*)c->d_err + kWorkOff);
   return EPIC_OK;
 }
 
@@ -939,6 +976,35 @@ WsArgs ws_args(const epic_ctx* c, void* ws) {
   a.snap_bytes = c->snap_bytes;
   return a;
 }
+
+// The context's tables with the work counters of kernel kind kid.
+DevTab tab_for(const epic_ctx* c, int kid) {
+  DevTab t = c->tab;
+  t.work = (unsigned long long*)((char*)c->d_err + kWorkOff) + (size_t)kid * 8;
+  return t;
+}
+
+// Brackets one kernel launch with HIP events on its stream when the
+// context's timing diagnostics are on.
+struct KernelTimer {
+  epic_ctx* c;
+  int kid;
+  hipStream_t s;
+  hipEvent_t a = nullptr, b = nullptr;
+  KernelTimer(epic_ctx* c_, int kid_, hipStream_t s_) : c(c_), kid(kid_), s(s_) {
+    if (!c->timing) return;
+    if (hipEventCreate(&a) != hipSuccess || hipEventCreate(&b) != hipSuccess) {
+      a = b = nullptr;
+      return;
+    }
+    (void)hipEventRecord(a, s);
+  }
+  ~KernelTimer() {
+    if (!a) return;
+    (void)hipEventRecord(b, s);
+    c->pending.push_back({kid, a, b});
+  }
+};
 
 }  // namespace
 
@@ -966,32 +1032,43 @@ struct FallbackLaunch {
 };
 
 #ifdef EPIC_KERNEL_UNIT
+// Base walks of sequences 0..B-1 (gb = B: Earley graphs; 2B: also the cover
+// graphs).
+template <int W>
+void launch_base(epic_ctx* c, const int32_t* seqs, int B, int n, int gb, const WsArgs& wa, hipStream_t stream) {
+  KernelTimer kt(c, kKBase, stream);
+  const DevTab tb = tab_for(c, kKBase);
+  if (W >= 16 && gb <= c->num_cus)
+    hipLaunchKernelGGL((base_kernel<W, kThreadsWide>), dim3(gb), dim3(kThreadsWide), 0, stream, tb, seqs, B, n, c->tag,
+                       wa);
+  else
+    hipLaunchKernelGGL((base_kernel<W, kThreads>), dim3(gb), dim3(kThreads), 0, stream, tb, seqs, B, n, c->tag, wa);
+}
+
 template <int W>
 epic_status ValidateLaunch<W>::run(epic_ctx* c, const int32_t* seqs, int B, int n, const int32_t* cs,
                                    const int32_t* cp, const int32_t* ct, int C, uint8_t* verdict, void* ws,
                                    hipStream_t stream) {
   int grid = std::min(C, c->nslot);
   const WsArgs wa = ws_args(c, ws);
+  const DevTab tb = tab_for(c, kKValidate);
   if ((grid > c->num_cus || n >= kShareSelectLen) && B <= c->base_slots) {
     // more walks than CUs, or long sequences: the chart up to each
     // candidate's masked run is its sequence's, walked by a base walk
     // (prefix sharing; long sequences also walk their cover graphs, which
     // the selection then reuses)
-    const int gb = n >= kShareSelectLen ? 2 * B : B;
-    if (W >= 16 && gb <= c->num_cus)
-      hipLaunchKernelGGL((base_kernel<W, kThreadsWide>), dim3(gb), dim3(kThreadsWide), 0, stream, c->tab, seqs, B, n,
-                         c->tag, wa);
-    else
-      hipLaunchKernelGGL((base_kernel<W, kThreads>), dim3(gb), dim3(kThreads), 0, stream, c->tab, seqs, B, n, c->tag,
-                         wa);
-    hipLaunchKernelGGL((validate_kernel<W, kThreads, true>), dim3(grid), dim3(kThreads), 0, stream, c->tab, seqs, B,
-                       n, cs, cp, ct, C, verdict, wa);
+    launch_base<W>(c, seqs, B, n, n >= kShareSelectLen ? 2 * B : B, wa, stream);
+    KernelTimer kt(c, kKValidate, stream);
+    hipLaunchKernelGGL((validate_kernel<W, kThreads, true>), dim3(grid), dim3(kThreads), 0, stream, tb, seqs, B, n, cs,
+                       cp, ct, C, verdict, wa);
   } else if (W >= 16 && grid <= c->num_cus) {
-    hipLaunchKernelGGL((validate_kernel<W, kThreadsWide, false>), dim3(grid), dim3(kThreadsWide), 0, stream, c->tab,
-                       seqs, B, n, cs, cp, ct, C, verdict, wa);
+    KernelTimer kt(c, kKValidate, stream);
+    hipLaunchKernelGGL((validate_kernel<W, kThreadsWide, false>), dim3(grid), dim3(kThreadsWide), 0, stream, tb, seqs,
+                       B, n, cs, cp, ct, C, verdict, wa);
   } else {
-    hipLaunchKernelGGL((validate_kernel<W, kThreads, false>), dim3(grid), dim3(kThreads), 0, stream, c->tab, seqs, B,
-                       n, cs, cp, ct, C, verdict, wa);
+    KernelTimer kt(c, kKValidate, stream);
+    hipLaunchKernelGGL((validate_kernel<W, kThreads, false>), dim3(grid), dim3(kThreads), 0, stream, tb, seqs, B, n, cs,
+                       cp, ct, C, verdict, wa);
   }
   return hipGetLastError() == hipSuccess ? EPIC_OK : EPIC_ERR_HIP;
 }
@@ -1009,28 +1086,26 @@ epic_status SelectLaunch<W>::run(epic_ctx* c, const int32_t* seqs, int B, int n,
   const WsArgs wa = ws_args(c, ws);
   // long sequences: Alg. 4's checks resume from base walks of both graphs
   const int share = n >= kShareSelectLen && B <= c->base_slots;
-  if (share) {
-    if (W >= 16 && 2 * B <= c->num_cus)
-      hipLaunchKernelGGL((base_kernel<W, kThreadsWide>), dim3(2 * B), dim3(kThreadsWide), 0, stream, c->tab, seqs, B,
-                         n, c->tag, wa);
-    else
-      hipLaunchKernelGGL((base_kernel<W, kThreads>), dim3(2 * B), dim3(kThreads), 0, stream, c->tab, seqs, B, n,
-                         c->tag, wa);
+  if (share) launch_base<W>(c, seqs, B, n, 2 * B, wa, stream);
+  {
+    KernelTimer kt(c, kKSpecClear, stream);
+    hipLaunchKernelGGL(spec_clear_kernel<W>, dim3((B * kSpec + 255) / 256), dim3(256), 0, stream, spec, B * kSpec);
   }
-  hipLaunchKernelGGL(spec_clear_kernel<W>, dim3((B * kSpec + 255) / 256), dim3(256), 0, stream, spec, B * kSpec);
   const bool wide = W >= 16 && grid <= c->num_cus;
+  const DevTab tb = tab_for(c, kKSelect);
+  KernelTimer kt(c, kKSelect, stream);
   if (wide && share)
-    hipLaunchKernelGGL((select_kernel<W, kThreadsWide, true>), dim3(grid), dim3(kThreadsWide), 0, stream, c->tab,
-                       seqs, B, n, cs, cp, ct, conf, verdict, C, sel, (long long*)counts, spec, wa);
-  else if (wide)
-    hipLaunchKernelGGL((select_kernel<W, kThreadsWide, false>), dim3(grid), dim3(kThreadsWide), 0, stream, c->tab,
-                       seqs, B, n, cs, cp, ct, conf, verdict, C, sel, (long long*)counts, spec, wa);
-  else if (share)
-    hipLaunchKernelGGL((select_kernel<W, kThreads, true>), dim3(grid), dim3(kThreads), 0, stream, c->tab, seqs, B, n,
-                       cs, cp, ct, conf, verdict, C, sel, (long long*)counts, spec, wa);
-  else
-    hipLaunchKernelGGL((select_kernel<W, kThreads, false>), dim3(grid), dim3(kThreads), 0, stream, c->tab, seqs, B,
+    hipLaunchKernelGGL((select_kernel<W, kThreadsWide, true>), dim3(grid), dim3(kThreadsWide), 0, stream, tb, seqs, B,
                        n, cs, cp, ct, conf, verdict, C, sel, (long long*)counts, spec, wa);
+  else if (wide)
+    hipLaunchKernelGGL((select_kernel<W, kThreadsWide, false>), dim3(grid), dim3(kThreadsWide), 0, stream, tb, seqs,
+                       B, n, cs, cp, ct, conf, verdict, C, sel, (long long*)counts, spec, wa);
+  else if (share)
+    hipLaunchKernelGGL((select_kernel<W, kThreads, true>), dim3(grid), dim3(kThreads), 0, stream, tb, seqs, B, n, cs,
+                       cp, ct, conf, verdict, C, sel, (long long*)counts, spec, wa);
+  else
+    hipLaunchKernelGGL((select_kernel<W, kThreads, false>), dim3(grid), dim3(kThreads), 0, stream, tb, seqs, B, n, cs,
+                       cp, ct, conf, verdict, C, sel, (long long*)counts, spec, wa);
   return hipGetLastError() == hipSuccess ? EPIC_OK : EPIC_ERR_HIP;
 }
 
@@ -1040,8 +1115,9 @@ epic_status FallbackLaunch<W>::run(epic_ctx* c, const int32_t* seqs, int B, int 
                                    const uint8_t* sel, const int32_t* num_commit, int C, uint8_t* accepted,
                                    void* ws, hipStream_t stream) {
   const int grid = std::min(B, c->nslot);
-  hipLaunchKernelGGL((fallback_kernel<W, kThreads>), dim3(grid), dim3(kThreads), 0, stream, c->tab, seqs, B, n, cs,
-                     cp, ct, conf, verdict, sel, num_commit, C, accepted, ws_args(c, ws));
+  KernelTimer kt(c, kKFallback, stream);
+  hipLaunchKernelGGL((fallback_kernel<W, kThreads>), dim3(grid), dim3(kThreads), 0, stream, tab_for(c, kKFallback),
+                     seqs, B, n, cs, cp, ct, conf, verdict, sel, num_commit, C, accepted, ws_args(c, ws));
   return hipGetLastError() == hipSuccess ? EPIC_OK : EPIC_ERR_HIP;
 }
 
@@ -1064,12 +1140,55 @@ epic_status dispatch_w(int W, Args... args) {
 
 extern "C" {
 
+static epic_status read_counters(epic_ctx* c, hipStream_t stream, int64_t* sets) {
+  if (hipStreamSynchronize(stream) != hipSuccess) return EPIC_ERR_HIP;
+  if (hipMemcpy(sets, (char*)c->d_err + kWorkOff, kKernelKinds * 8 * sizeof(int64_t), hipMemcpyDeviceToHost) !=
+      hipSuccess)
+    return EPIC_ERR_HIP;
+  if (hipMemset((char*)c->d_err + kWorkOff, 0, kKernelKinds * 8 * sizeof(int64_t)) != hipSuccess) return EPIC_ERR_HIP;
+  return EPIC_OK;
+}
+
 epic_status epic_ctx_work_counters(epic_ctx* c, hipStream_t stream, int64_t* out) {
   if (!c || !out) return EPIC_ERR_NULL;
-  if (hipStreamSynchronize(stream) != hipSuccess) return EPIC_ERR_HIP;
-  if (hipMemcpy(out, (char*)c->d_err + 64, 6 * sizeof(int64_t), hipMemcpyDeviceToHost) != hipSuccess)
-    return EPIC_ERR_HIP;
-  if (hipMemset((char*)c->d_err + 64, 0, 6 * sizeof(int64_t)) != hipSuccess) return EPIC_ERR_HIP;
+  int64_t sets[kKernelKinds * 8];
+  epic_status s = read_counters(c, stream, sets);
+  if (s != EPIC_OK) return s;
+  for (int i = 0; i < kWorkCounters; ++i) {
+    out[i] = 0;
+    for (int k = 0; k < kKernelKinds; ++k) out[i] += sets[k * 8 + i];
+  }
+  return EPIC_OK;
+}
+
+epic_status epic_ctx_set_timing(epic_ctx* c, int32_t enable) {
+  if (!c) return EPIC_ERR_NULL;
+  c->timing = enable != 0;
+  return EPIC_OK;
+}
+
+epic_status epic_ctx_kernel_stats(epic_ctx* c, hipStream_t stream, double* ms, int64_t* launches, int64_t* work) {
+  if (!c || !ms || !launches || !work) return EPIC_ERR_NULL;
+  int64_t sets[kKernelKinds * 8];
+  epic_status s = read_counters(c, stream, sets);
+  if (s != EPIC_OK) return s;
+  for (auto& p : c->pending) {
+    float t = 0.f;
+    if (hipEventSynchronize(p.b) == hipSuccess && hipEventElapsedTime(&t, p.a, p.b) == hipSuccess) {
+      c->kernel_ms[p.kid] += t;
+      c->kernel_launches[p.kid] += 1;
+    }
+    (void)hipEventDestroy(p.a);
+    (void)hipEventDestroy(p.b);
+  }
+  c->pending.clear();
+  for (int k = 0; k < kKernelKinds; ++k) {
+    ms[k] = c->kernel_ms[k];
+    launches[k] = c->kernel_launches[k];
+    c->kernel_ms[k] = 0;
+    c->kernel_launches[k] = 0;
+    for (int i = 0; i < kWorkCounters; ++i) work[k * kWorkCounters + i] = sets[k * 8 + i];
+  }
   return EPIC_OK;
 }
 
@@ -1134,10 +1253,6 @@ epic_status epic_ctx_create(const epic_lexer_desc* lexer, const epic_grammar_des
   c->off_bseq = c->off_snap + c->snap_bytes * 2 * c->base_slots;
   c->off_spec = c->off_bseq + align256((size_t)2 * c->base_slots * max_seq_len * 4);
   c->ws_bytes = c->off_spec + align256((size_t)c->max_batch * kSpec * 8);  // + speculated checks
-  {
-    static std::atomic<uint64_t> counter{1};
-    c->tag = (counter.fetch_add(1) << 32) ^ (uint64_t)(uintptr_t)c ^ 0x9E3779B97F4A7C15ull;
-  }
   epic_status s = upload(c);
   if (s != EPIC_OK) {
     epic_ctx_destroy(c);
@@ -1149,6 +1264,10 @@ epic_status epic_ctx_create(const epic_lexer_desc* lexer, const epic_grammar_des
 
 void epic_ctx_destroy(epic_ctx* c) {
   if (!c) return;
+  for (auto& p : c->pending) {
+    (void)hipEventDestroy(p.a);
+    (void)hipEventDestroy(p.b);
+  }
   if (c->d_tables) (void)hipFree(c->d_tables);
   if (c->d_memo) (void)hipFree(c->d_memo);
   if (c->d_err) (void)hipFree(c->d_err);
@@ -1165,7 +1284,10 @@ epic_status epic_lexmemo_build(epic_ctx* c, hipStream_t stream) {
   if (!c) return EPIC_ERR_NULL;
   const size_t total = (size_t)c->H.V * c->H.Q;
   const unsigned grid = (unsigned)((total + kMemoThreads - 1) / kMemoThreads);
-  hipLaunchKernelGGL(lexmemo_kernel, dim3(grid), dim3(kMemoThreads), 0, stream, c->tab, c->d_memo);
+  {
+    KernelTimer kt(c, kKLexmemo, stream);
+    hipLaunchKernelGGL(lexmemo_kernel, dim3(grid), dim3(kMemoThreads), 0, stream, c->tab, c->d_memo);
+  }
   if (hipGetLastError() != hipSuccess) return EPIC_ERR_HIP;
   c->memo_built = true;
   return EPIC_OK;

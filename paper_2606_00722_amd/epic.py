@@ -25,7 +25,9 @@ DEV_BAD_CANDIDATE, DEV_CAPACITY, DEV_BAD_SELECT = 1, 2, 4
 FUNCTIONS = ["epic_ctx_create", "epic_ctx_destroy", "epic_workspace_bytes", "epic_gap_classes", "epic_item_words",
              "epic_lexmemo_build", "epic_memo_export", "epic_validate_batch", "epic_select_compatible",
              "epic_commit_fallback",
-             "epic_ctx_device_error", "epic_ctx_work_counters", "epic_status_string"]
+             "epic_ctx_device_error", "epic_ctx_work_counters", "epic_ctx_set_timing", "epic_ctx_kernel_stats",
+             "epic_status_string"]
+KERNEL_KINDS = ["lexmemo", "base", "validate", "select", "fallback", "spec_clear"]
 
 
 class EpicError(RuntimeError):
@@ -82,6 +84,10 @@ def lib() -> ctypes.CDLL:
         L.epic_ctx_device_error.restype = ctypes.c_int
         L.epic_ctx_work_counters.argtypes = [P, P, P]
         L.epic_ctx_work_counters.restype = ctypes.c_int
+        L.epic_ctx_set_timing.argtypes = [P, i32]
+        L.epic_ctx_set_timing.restype = ctypes.c_int
+        L.epic_ctx_kernel_stats.argtypes = [P, P, P, P, P]
+        L.epic_ctx_kernel_stats.restype = ctypes.c_int
         L.epic_status_string.argtypes = [ctypes.c_int]
         L.epic_status_string.restype = ctypes.c_char_p
         _lib = L
@@ -152,9 +158,10 @@ class Context:
         return int(lib().epic_gap_classes(self._h))
 
     def alloc_workspace(self, device="cuda"):
+        """A zeroed workspace (a fresh workspace must hold no walk records)."""
         import torch
 
-        return torch.empty(self.workspace_bytes + 256, dtype=torch.uint8, device=device)
+        return torch.zeros(self.workspace_bytes + 256, dtype=torch.uint8, device=device)
 
     def lexmemo_build(self, stream=None):
         _check("epic_lexmemo_build", lib().epic_lexmemo_build(self._h, _stream(stream)))
@@ -199,6 +206,20 @@ class Context:
         out = np.zeros(6, dtype=np.int64)
         _check("epic_ctx_work_counters", lib().epic_ctx_work_counters(self._h, _stream(stream), out.ctypes.data))
         return out
+
+    def set_timing(self, enable: bool = True):
+        _check("epic_ctx_set_timing", lib().epic_ctx_set_timing(self._h, int(bool(enable))))
+
+    def kernel_stats(self, stream=None) -> dict:
+        """Per kernel kind (KERNEL_KINDS): summed event ms, launches and the
+        int64[6] work counters of its walks (read and cleared)."""
+        ms = np.zeros(6, dtype=np.float64)
+        n = np.zeros(6, dtype=np.int64)
+        work = np.zeros(36, dtype=np.int64)
+        _check("epic_ctx_kernel_stats", lib().epic_ctx_kernel_stats(self._h, _stream(stream), ms.ctypes.data,
+                                                                    n.ctypes.data, work.ctypes.data))
+        return {k: {"ms": float(ms[i]), "launches": int(n[i]), "work": work[6 * i:6 * i + 6].copy()}
+                for i, k in enumerate(KERNEL_KINDS)}
 
     @property
     def item_words(self) -> int:

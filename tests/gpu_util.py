@@ -42,3 +42,13 @@ class Gpu:
 
     def errors(self) -> int:
         return self.ctx.device_error()
+
+    def fallback(self, seqs, seq, pos, tok, conf, verdict, selected, num_commit) -> np.ndarray:
+        torch = self.torch
+        C = len(seq)
+        out = torch.full((max(C, 1),), 7, dtype=torch.uint8, device=self.dev)
+        self.ctx.fallback(self.t(seqs), self.t(seq), self.t(pos), self.t(tok), self.t(conf, torch.float32),
+                          self.t(verdict, torch.uint8), self.t(selected, torch.uint8), self.t(num_commit),
+                          out[:C], self.ws)
+        torch.cuda.synchronize()
+        return out[:C].cpu().numpy()
