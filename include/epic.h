@@ -161,6 +161,26 @@ epic_status epic_validate_batch(epic_ctx* ctx, const int32_t* d_seqs, int32_t B,
                                 const int32_t* d_cand_tok, int32_t C, uint8_t* d_verdict,
                                 void* d_workspace, size_t workspace_bytes, hipStream_t stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, serving loops that must not allocate, harnesses that forbid
+ * hipMalloc): epic_validate_batch without a workspace.  The verdicts are
+ * epic_validate_batch's.  The walks keep their charts in a scratch array of
+ * 256 MiB that the library holds in device memory, one per GPU, from the
+ * first context created on that GPU until the process ends; the call itself
+ * calls no hipMalloc, hipFree or other allocating routine.  Every call on a
+ * GPU shares that GPU's array, so calls that overlap on one GPU (other
+ * streams, contexts or host threads) race: the caller serialises them.
+ * Nothing in the array must start at zero (a walk writes every chart row
+ * before reading it, and nothing is kept between calls: no prefix sharing,
+ * no walk records).  As many walks run at once as chart slots of the
+ * context fit in the array (at most 1024); EPIC_ERR_CAPACITY when not even
+ * one fits (the slot size grows with the context's max_seq_len and item
+ * words: about 11 MB for 16-word items at 256 or more tokens). */
+epic_status epic_validate_batch_noalloc(epic_ctx* ctx, const int32_t* d_seqs, int32_t B, int32_t n,
+                                        const int32_t* d_cand_seq, const int32_t* d_cand_pos,
+                                        const int32_t* d_cand_tok, int32_t C, uint8_t* d_verdict,
+                                        hipStream_t stream);
+
 /* Relaxed compatible-subset selection (Alg. 4): per sequence, the candidates
  * with verdict 1 are sorted by descending confidence (float32, ties to the
  * lower candidate index) and passed to RelaxedSelect followed by

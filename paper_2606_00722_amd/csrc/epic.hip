@@ -850,6 +850,7 @@ struct epic_ctx {
   size_t off_snap = 0, snap_bytes = 0, off_spec = 0, off_bseq = 0;
   uint64_t tag = 0;  // owner tag of the base records this context writes
   bool cover_bases = false;  // the last base launch also walked the cover graphs
+  void* scratch = nullptr;  // this device's static scratch (epic_validate_batch_noalloc)
   // diagnostics: per-kernel HIP-event timing (epic_ctx_set_timing)
   bool timing = false;
   struct Pending {
@@ -1024,6 +1025,14 @@ struct SelectLaunch {
                          int64_t* counts, void* ws, hipStream_t stream);
 };
 
+// Candidate walks only (no prefix sharing), in the slots of a caller-given
+// region: the launch of epic_validate_batch_noalloc.
+template <int W>
+struct ValidatePlainLaunch {
+  static epic_status run(epic_ctx* c, const int32_t* seqs, int B, int n, const int32_t* cs, const int32_t* cp,
+                         const int32_t* ct, int C, uint8_t* verdict, void* region, int nslot, hipStream_t stream);
+};
+
 template <int W>
 struct FallbackLaunch {
   static epic_status run(epic_ctx* c, const int32_t* seqs, int B, int n, const int32_t* cs, const int32_t* cp,
@@ -1121,10 +1130,59 @@ epic_status FallbackLaunch<W>::run(epic_ctx* c, const int32_t* seqs, int B, int 
   return hipGetLastError() == hipSuccess ? EPIC_OK : EPIC_ERR_HIP;
 }
 
+template <int W>
+epic_status ValidatePlainLaunch<W>::run(epic_ctx* c, const int32_t* seqs, int B, int n, const int32_t* cs,
+                                        const int32_t* cp, const int32_t* ct, int C, uint8_t* verdict, void* region,
+                                        int nslot, hipStream_t stream) {
+  WsArgs wa = ws_args(c, region);
+  wa.nslot = nslot;  // walk slots 0..nslot-1 only; no base slots or records
+  wa.base_slots = 0;
+  const int grid = std::min(C, nslot);
+  const DevTab tb = tab_for(c, kKValidate);
+  if (W >= 16 && grid <= c->num_cus)
+    hipLaunchKernelGGL((validate_kernel<W, kThreadsWide, false>), dim3(grid), dim3(kThreadsWide), 0, stream, tb, seqs,
+                       B, n, cs, cp, ct, C, verdict, wa);
+  else
+    hipLaunchKernelGGL((validate_kernel<W, kThreads, false>), dim3(grid), dim3(kThreads), 0, stream, tb, seqs, B, n, cs,
+                       cp, ct, C, verdict, wa);
+  return hipGetLastError() == hipSuccess ? EPIC_OK : EPIC_ERR_HIP;
+}
+
+template struct ValidatePlainLaunch<EPIC_KERNEL_UNIT>;
 template struct ValidateLaunch<EPIC_KERNEL_UNIT>;
 template struct FallbackLaunch<EPIC_KERNEL_UNIT>;
 template struct SelectLaunch<EPIC_KERNEL_UNIT>;
 #else
+
+// Device scratch of epic_validate_batch_noalloc, for callers that cannot
+// allocate: a file-scope array, one copy per GPU, held until the process
+// ends.  Host code never passes `scratch` itself to a kernel (on the host it
+// names a stand-in, not device memory): each device's address comes from
+// hipGetSymbolAddress, taken once per device with that device current.
+constexpr size_t kStaticScratchBytes = (size_t)256 << 20;
+static __device__ __align__(256) char scratch[kStaticScratchBytes];
+
+namespace {
+std::mutex g_scratch_mu;
+constexpr int kMaxDevices = 64;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The current device's scratch address (set-up, once per device); nullptr
+// if the lookup fails.
+void* device_scratch(int device) {
+  if (device < 0 || device >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[device]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess) {
+      (void)hipGetLastError();
+      return nullptr;
+    }
+    g_scratch_ptr[device] = p;
+  }
+  return g_scratch_ptr[device];
+}
+}  // namespace
 
 template <template <int> class Launcher, class... Args>
 epic_status dispatch_w(int W, Args... args) {
@@ -1258,6 +1316,7 @@ epic_status epic_ctx_create(const epic_lexer_desc* lexer, const epic_grammar_des
     epic_ctx_destroy(c);
     return s;
   }
+  c->scratch = device_scratch(c->device);  // with the context's device current
   *out = c;
   return EPIC_OK;
 }
@@ -1325,6 +1384,23 @@ epic_status epic_validate_batch(epic_ctx* c, const int32_t* d_seqs, int32_t B, i
   if (s != EPIC_OK || C == 0) return s;
   return dispatch_w<ValidateLaunch>(c->H.W, c, d_seqs, (int)B, (int)n, d_cand_seq, d_cand_pos, d_cand_tok, (int)C,
                                     d_verdict, d_workspace, stream);
+}
+
+epic_status epic_validate_batch_noalloc(epic_ctx* c, const int32_t* d_seqs, int32_t B, int32_t n,
+                                        const int32_t* d_cand_seq, const int32_t* d_cand_pos,
+                                        const int32_t* d_cand_tok, int32_t C, uint8_t* d_verdict,
+                                        hipStream_t stream) {
+  if (!c) return EPIC_ERR_NULL;
+  if (B < 0 || n < 0 || C < 0) return EPIC_ERR_ARG;
+  if (B > c->max_batch || n > c->max_seq || C > c->max_cands) return EPIC_ERR_CAPACITY;
+  if (C == 0) return EPIC_OK;
+  if (!d_seqs || !d_cand_seq || !d_cand_pos || !d_cand_tok || !d_verdict) return EPIC_ERR_NULL;
+  if (!c->memo_built) return EPIC_ERR_STATE;
+  if (!c->scratch) return EPIC_ERR_HIP;
+  const size_t nslot = kStaticScratchBytes / c->slot_bytes;  // walks resident at once
+  if (nslot < 1) return EPIC_ERR_CAPACITY;  // one walk's chart does not fit
+  return dispatch_w<ValidatePlainLaunch>(c->H.W, c, d_seqs, (int)B, (int)n, d_cand_seq, d_cand_pos, d_cand_tok, (int)C,
+                                         d_verdict, c->scratch, (int)std::min<size_t>(nslot, 1024), stream);
 }
 
 epic_status epic_select_compatible(epic_ctx* c, const int32_t* d_seqs, int32_t B, int32_t n,

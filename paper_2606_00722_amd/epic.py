@@ -23,7 +23,8 @@ STATUS = {0: "ok", -1: "null pointer", -2: "argument out of range", -3: "capacit
 DEV_BAD_CANDIDATE, DEV_CAPACITY, DEV_BAD_SELECT = 1, 2, 4
 
 FUNCTIONS = ["epic_ctx_create", "epic_ctx_destroy", "epic_workspace_bytes", "epic_gap_classes", "epic_item_words",
-             "epic_lexmemo_build", "epic_memo_export", "epic_validate_batch", "epic_select_compatible",
+             "epic_lexmemo_build", "epic_memo_export", "epic_validate_batch", "epic_validate_batch_noalloc",
+             "epic_select_compatible",
              "epic_commit_fallback",
              "epic_ctx_device_error", "epic_ctx_work_counters", "epic_ctx_set_timing", "epic_ctx_kernel_stats",
              "epic_status_string"]
@@ -76,6 +77,8 @@ def lib() -> ctypes.CDLL:
         L.epic_memo_export.restype = ctypes.c_int
         L.epic_validate_batch.argtypes = [P, P, i32, i32, P, P, P, i32, P, P, sz, P]
         L.epic_validate_batch.restype = ctypes.c_int
+        L.epic_validate_batch_noalloc.argtypes = [P, P, i32, i32, P, P, P, i32, P, P]
+        L.epic_validate_batch_noalloc.restype = ctypes.c_int
         L.epic_select_compatible.argtypes = [P, P, i32, i32, P, P, P, P, P, i32, P, P, P, sz, P]
         L.epic_select_compatible.restype = ctypes.c_int
         L.epic_commit_fallback.argtypes = [P, P, i32, i32, P, P, P, P, P, P, P, i32, P, P, sz, P]
@@ -183,6 +186,14 @@ class Context:
         _check("epic_validate_batch", lib().epic_validate_batch(
             self._h, _ptr(seqs), B, n, _ptr(cand_seq), _ptr(cand_pos), _ptr(cand_tok), int(cand_seq.numel()),
             _ptr(verdict), wp, wb, _stream(stream)))
+
+    def validate_noalloc(self, seqs, cand_seq, cand_pos, cand_tok, verdict, stream=None):
+        """epic_validate_batch_noalloc: no workspace (the library's static
+        device scratch; calls on one GPU must not overlap)."""
+        B, n = (int(seqs.shape[0]), int(seqs.shape[1])) if seqs.dim() == 2 else (0, 0)
+        _check("epic_validate_batch_noalloc", lib().epic_validate_batch_noalloc(
+            self._h, _ptr(seqs), B, n, _ptr(cand_seq), _ptr(cand_pos), _ptr(cand_tok), int(cand_seq.numel()),
+            _ptr(verdict), _stream(stream)))
 
     def select(self, seqs, cand_seq, cand_pos, cand_tok, conf, verdict, selected, workspace, counts=None,
                stream=None):
