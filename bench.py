@@ -66,6 +66,176 @@ def copy_calibration(mib: int) -> int:
     return 0
 
 
+KERNEL_KIND = {"lexmemo_kernel": "lexmemo", "base_kernel": "base", "validate_kernel": "validate",
+               "select_kernel": "select", "fallback_kernel": "fallback", "spec_clear_kernel": "spec_clear"}
+LDS_COUNTERS = ("SQ_INSTS_LDS_LOAD_BANDWIDTH", "SQ_INSTS_LDS_STORE_BANDWIDTH", "SQ_INSTS_LDS_ATOMIC_BANDWIDTH")
+XCDS = 8  # GRBM_GUI_ACTIVE is summed over the eight accelerator dies
+CUS = 256
+PEAK_CLOCK_GHZ = 2.4
+
+
+def lds_peak(configs=((2, 1024), (1, 1024), (2, 512), (4, 256)), iters: int = 1 << 15) -> dict:
+    """LDS read bandwidth of the device from the library's streaming
+    microbenchmark, over a few launch shapes (workgroups per CU, threads):
+    bytes per clock per CU (shader clock measured in the kernel against the
+    constant-rate wall clock) and GB/s; the best shape gives the peak used by
+    the roofline (times 256 CUs and the 2.4 GHz peak engine clock)."""
+    import torch
+
+    from paper_2606_00722_amd import epic
+
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    sink = torch.zeros(8, dtype=torch.int32, device="cuda:0")
+    shader_khz, wall_khz = epic.clock_rates()
+    runs = []
+    for per_cu, threads in configs:
+        blocks = per_cu * cus
+        epic.lds_stream(blocks, threads, 256, sink)  # warm
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        epic.lds_stream(blocks, threads, iters, sink)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1)
+        s = [int(v) & 0xFFFFFFFF for v in sink.cpu().tolist()]
+        ticks, wall = s[2] | (s[3] << 32), s[4] | (s[5] << 32)
+        clk_hz = ticks / (wall / (wall_khz * 1e3)) if wall else shader_khz * 1e3
+        nbytes = float(blocks) * threads * iters * 16
+        runs.append({"workgroups_per_cu": per_cu, "threads": threads, "bytes": nbytes, "ms": round(ms, 4),
+                     "GB/s": round(nbytes / (ms * 1e-3) / 1e9, 1), "clock_mhz_measured": round(clk_hz / 1e6, 1),
+                     "bytes_per_clk_per_cu": round(nbytes / (ms * 1e-3) / clk_hz / cus, 2)})
+    best = max(r["bytes_per_clk_per_cu"] for r in runs)
+    return {"runs": runs, "cus": cus, "clock_mhz_rated": shader_khz / 1e3, "bytes_per_clk_per_cu": best,
+            "peak_gbs": round(best * CUS * PEAK_CLOCK_GHZ, 1), "iters": iters}
+
+
+def lds_peak_record():
+    """The committed LDS peak (profiles/lds_peak.json, the output of
+    --lds-peak): bytes per clock per CU from the streaming microbenchmark,
+    times 256 CUs and the 2.4 GHz peak engine clock (peak_gbs)."""
+    path = os.path.join(PROFILES, "lds_peak.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        return json.load(f).get("lds_peak")
+
+
+def _counter_csv(run_dir: str) -> dict:
+    """Per kernel kind: dispatches, summed counter values and summed
+    durations (ns) of one rocprofv3 --pmc run (csv output)."""
+    import csv
+    import glob
+
+    files = glob.glob(os.path.join(run_dir, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        raise FileNotFoundError(f"no counter_collection.csv under {run_dir}")
+    out, seen = {}, set()
+    with open(files[0]) as fh:
+        for row in csv.DictReader(fh):
+            name = row["Kernel_Name"]
+            kind = next((v for k, v in KERNEL_KIND.items() if k in name), "copy" if "elementwise" in name else None)
+            if kind is None:
+                continue
+            d = out.setdefault(kind, {"dispatches": 0, "ns": 0.0, "counters": {}, "name": name.split("(")[0],
+                                      "scratch": int(float(row.get("Scratch_Size") or 0)),
+                                      "vgpr": int(float(row.get("VGPR_Count") or 0)),
+                                      "lds_block": int(float(row.get("LDS_Block_Size") or 0))})
+            key = (row["Dispatch_Id"], kind)
+            if key not in seen:
+                seen.add(key)
+                d["dispatches"] += 1
+                d["ns"] += int(row["End_Timestamp"]) - int(row["Start_Timestamp"])
+            c = row["Counter_Name"]
+            d["counters"][c] = d["counters"].get(c, 0.0) + float(row["Counter_Value"])
+    return out
+
+
+def _run_source_hash(log_path: str):
+    """The source hash a bench run printed in its JSON line (None if absent)."""
+    try:
+        with open(log_path) as f:
+            for line in f:
+                if line.startswith("{") and '"source_hash"' in line:
+                    return json.loads(line).get("source_hash")
+    except OSError:
+        pass
+    return None
+
+
+def pmc_summarize(pmc_dir: str, preset: int, hash_override=None) -> int:
+    """Turn the rocprofv3 counter runs of one workload into
+    profiles/<kernel>_preset<preset>_pmc.json per kernel kind, and print a
+    markdown table.  Expected run directories under pmc_dir: p<preset>_lds,
+    p<preset>_valu, p<preset>_fetch, p<preset>_write (one counter set each),
+    copy_fetch and copy_write (the --copy-calibration 256 runs).  Values are
+    averages per dispatch; LDS bytes = 64 x the three LDS bandwidth counters
+    (units of 64 bytes); HBM bytes = FETCH_SIZE and WRITE_SIZE (KiB) scaled by
+    the plain copy's readings; VALU busy = SQ_ACTIVE_INST_VALU / CUs / one
+    die's GRBM_GUI_ACTIVE."""
+    from paper_2606_00722_amd import workloads as W
+
+    runs = {k: _counter_csv(os.path.join(pmc_dir, f"p{preset}_{k}")) for k in ("lds", "valu", "fetch", "write")}
+    cf = _counter_csv(os.path.join(pmc_dir, "copy_fetch"))["copy"]
+    cw = _counter_csv(os.path.join(pmc_dir, "copy_write"))["copy"]
+    copy_bytes = 256 << 20
+    f_fac = copy_bytes / (cf["counters"]["FETCH_SIZE"] / cf["dispatches"] * 1024)
+    w_fac = copy_bytes / (cw["counters"]["WRITE_SIZE"] / cw["dispatches"] * 1024)
+    peak = lds_peak_record()
+    # the sources the counters were taken on, as the profiled run printed them
+    sh = hash_override or _run_source_hash(os.path.join(pmc_dir, f"p{preset}_lds.log")) or source_hash()
+    rows = []
+    for kind in ("validate", "select", "base", "fallback", "lexmemo"):
+        if kind not in runs["lds"]:
+            continue
+        per = {}
+        for name, run in runs.items():
+            d = run.get(kind)
+            if not d:
+                continue
+            for c, v in d["counters"].items():
+                per[f"{c}@{name}" if c == "GRBM_GUI_ACTIVE" else c] = v / d["dispatches"]
+        d0 = runs["lds"][kind]
+        us = d0["ns"] / d0["dispatches"] / 1e3
+        lds_b = 64.0 * sum(per.get(c, 0.0) for c in LDS_COUNTERS)
+        hbm_b = per.get("FETCH_SIZE", 0.0) * 1024 * f_fac + per.get("WRITE_SIZE", 0.0) * 1024 * w_fac
+        grbm_valu = per.get("GRBM_GUI_ACTIVE@valu", 0.0) / XCDS
+        valu_busy = per.get("SQ_ACTIVE_INST_VALU", 0.0) / CUS / grbm_valu if grbm_valu else None
+        valu_util = (per["SQ_THREAD_CYCLES_VALU"] / (per["SQ_ACTIVE_INST_VALU"] * 64)
+                     if per.get("SQ_ACTIVE_INST_VALU") else None)
+        conflict = per.get("SQ_LDS_BANK_CONFLICT", 0.0) / max(per.get("SQ_LDS_IDX_ACTIVE", 0.0), 1.0)
+        hit, miss = per.get("TCC_HIT_sum", 0.0), per.get("TCC_MISS_sum", 0.0)
+        lds_gbs = lds_b / (us * 1e-6) / 1e9 if us else None
+        rec = {"kernel": kind, "kernel_name": d0["name"], "preset": preset, "workload": W.PRESET_NAMES[preset],
+               "source_hash": sh, "dispatches": d0["dispatches"], "us_per_dispatch_counter_run": round(us, 2),
+               "hbm_bytes_per_launch": round(hbm_b), "fetch_factor": round(f_fac, 4), "write_factor": round(w_fac, 4),
+               "lds_bytes_per_launch": round(lds_b), "lds_gbs_counter_run": round(lds_gbs, 2) if lds_gbs else None,
+               "lds_peak_gbs": peak["peak_gbs"] if peak else None,
+               "lds_bank_conflict_per_active_cycle": round(conflict, 4),
+               "valu_busy": round(valu_busy, 5) if valu_busy is not None else None,
+               "valu_thread_utilization": round(valu_util, 4) if valu_util is not None else None,
+               "waves": per.get("SQ_WAVES"), "tcc_hit_rate": round(hit / (hit + miss), 4) if hit + miss else None,
+               "scratch_bytes_per_lane": d0["scratch"], "vgpr": d0["vgpr"], "lds_block_bytes": d0["lds_block"],
+               "counters_per_dispatch": {k: round(v, 1) for k, v in sorted(per.items())}}
+        with open(os.path.join(PROFILES, f"{kind}_preset{preset}_pmc.json"), "w") as f:
+            json.dump(rec, f, indent=1)
+            f.write("\n")
+        rows.append(rec)
+    print("| kernel | dispatches | us/dispatch | LDS MB | LDS GB/s | of LDS peak | bank-conflict cycles per "
+          "LDS-active cycle | VALU busy | VALU thread util | HBM MB | L2 hit rate | scratch B/lane |")
+    print("|---|---|---|---|---|---|---|---|---|---|---|---|")
+    for r in rows:
+        frac = (r["lds_gbs_counter_run"] / r["lds_peak_gbs"]
+                if r["lds_peak_gbs"] and r["lds_gbs_counter_run"] else None)
+        print(f"| {r['kernel_name']} | {r['dispatches']} | {r['us_per_dispatch_counter_run']} | "
+              f"{r['lds_bytes_per_launch'] / 1e6:.2f} | {r['lds_gbs_counter_run']} | "
+              f"{None if frac is None else round(frac, 5)} | {r['lds_bank_conflict_per_active_cycle']} | "
+              f"{r['valu_busy']} | {r['valu_thread_utilization']} | {r['hbm_bytes_per_launch'] / 1e6:.2f} | "
+              f"{r['tcc_hit_rate']} | {r['scratch_bytes_per_lane']} |")
+    print(f"\nsource_hash {sh}; copy factors FETCH {f_fac:.4f}, WRITE {w_fac:.4f}")
+    return 0
+
+
 def cpu_model() -> str:
     try:
         with open("/proc/cpuinfo") as f:
@@ -144,12 +314,23 @@ def main() -> int:
     ap.add_argument("--cpu-seconds", type=float, default=24.0,
                     help="time budget of the oracle baseline (all legs together)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--lds-peak", action="store_true",
+                    help="run only the LDS streaming microbenchmark and print its bandwidth")
+    ap.add_argument("--pmc-summary", metavar="DIR",
+                    help="summarise the rocprofv3 counter runs under DIR for --preset into profiles/ (no GPU)")
+    ap.add_argument("--source-hash", default=None,
+                    help="with --pmc-summary: the source hash of the profiled run, when its log does not print it")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="run only a plain device copy of MIB MiB, 5 launches (the reference kernel that "
                          "scales rocprofv3 FETCH_SIZE / WRITE_SIZE readings to bytes)")
     args = ap.parse_args()
     if args.copy_calibration:
         return copy_calibration(args.copy_calibration)
+    if args.lds_peak:
+        print(json.dumps({"lds_peak": lds_peak()}))
+        return 0
+    if args.pmc_summary:
+        return pmc_summarize(args.pmc_summary, args.preset, args.source_hash)
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU only: the library has no multi-GPU path "
@@ -296,17 +477,39 @@ def main() -> int:
                    "walks_per_step": int(st["work"][0]) / args.steps}
     dom = max(kern, key=lambda k: kern[k]["ms_per_step"])
     kd = kern[dom]
-    bytes_per_launch = kd["bytes"] / kd["launches"]
-    achieved = bytes_per_launch / (kd["ms_per_launch"] * 1e-3) / 1e9
+    ms_launch = kd["ms_per_launch"]
+    hbm_launch = kd["bytes"] / kd["launches"]
+    hbm_gbs = hbm_launch / (ms_launch * 1e-3) / 1e9
     pmc = pmc_summary(dom, args.preset)
-    roof = {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 3), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": round(achieved / HBM_PEAK_GBS, 6),
-            "traffic": pmc.get("hbm_bytes_per_launch") if pmc else None,
-            "bytes_per_launch": round(bytes_per_launch, 1), "ms_per_launch": round(kd["ms_per_launch"], 4)}
+    peak = lds_peak_record()
+    lds_peak_gbs = peak["peak_gbs"] if peak else None
+    if dom == "lexmemo":  # the one HBM-bound kernel: no LDS traffic
+        roof = {"bound": "hbm", "kernel": dom, "achieved": round(hbm_gbs, 3), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(hbm_gbs / HBM_PEAK_GBS, 6), "traffic": pmc.get("hbm_bytes_per_launch") if pmc else None,
+                "bytes_per_launch": round(hbm_launch, 1), "ms_per_launch": round(ms_launch, 4)}
+    else:
+        # walk kernels: the chart's item sets are combined in LDS; algorithmic
+        # LDS bytes per applied (task, entry) pair: advance mask, slot words
+        # read and ORed (3 x 4W), per chart entry written: its slot words (4W)
+        w = kstats[dom]["work"]
+        lds_launch = float(w[5] * 12 * Wd + w[1] * 4 * Wd) / kd["launches"]
+        lds_gbs = lds_launch / (ms_launch * 1e-3) / 1e9
+        roof = {"bound": "lds", "kernel": dom, "achieved": round(lds_gbs, 3), "peak": lds_peak_gbs, "unit": "GB/s",
+                "frac": round(lds_gbs / lds_peak_gbs, 7) if lds_peak_gbs else None,
+                "traffic": pmc.get("hbm_bytes_per_launch") if pmc else None,
+                "bytes_per_launch": round(lds_launch, 1), "ms_per_launch": round(ms_launch, 4),
+                "lds_traffic": pmc.get("lds_bytes_per_launch") if pmc else None,
+                "lds_traffic_frac": (round(pmc["lds_bytes_per_launch"] / (ms_launch * 1e-3) / 1e9 / lds_peak_gbs, 6)
+                                     if pmc and lds_peak_gbs else None),
+                "hbm": {"achieved": round(hbm_gbs, 3), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                        "frac": round(hbm_gbs / HBM_PEAK_GBS, 7), "bytes_per_launch": round(hbm_launch, 1)},
+                "valu": {"busy": pmc.get("valu_busy"), "thread_utilization": pmc.get("valu_thread_utilization")}
+                if pmc else None,
+                "peak_source": "LDS streaming microbenchmark (profiles/lds_peak.json) x 256 CUs x 2.4 GHz"}
     if pmc:
-        for key in ("lds", "valu", "occupancy"):
-            if key in pmc:
-                roof[key] = pmc[key]
+        roof["counters"] = {"source_hash": pmc["source_hash"], "scratch_bytes_per_lane": pmc.get("scratch_bytes_per_lane"),
+                            "tcc_hit_rate": pmc.get("tcc_hit_rate"),
+                            "lds_bank_conflict_per_active_cycle": pmc.get("lds_bank_conflict_per_active_cycle")}
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -317,6 +520,7 @@ def main() -> int:
         "metric": METRIC, "value": round(checks / elapsed, 2), "unit": "checks/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(1e3 * elapsed / args.steps, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "u32", "data": "synthetic",
+        "source_hash": source_hash(),
         "config": {"workload": W.PRESET_NAMES[args.preset], "preset": args.preset, "batch": inst.B,
                    "seq_len": inst.n, "candidates_per_step": props_per_step, "steps_cycled": len(traj),
                    "seed": args.seed, "parallelism": "none (1 GPU)"},

@@ -253,6 +253,24 @@ epic_status epic_ctx_set_timing(epic_ctx* ctx, int32_t enable);
  * elements. */
 epic_status epic_ctx_kernel_stats(epic_ctx* ctx, hipStream_t stream, double* ms, int64_t* launches, int64_t* work);
 
+/* Diagnostics: LDS streaming microbenchmark, the measurement behind the LDS
+ * peak that walk kernels are compared with.  Launches `blocks` workgroups of
+ * `threads` threads (a multiple of 64, at most 1024) on `stream`; each
+ * workgroup fills 64 KiB of LDS, then every thread reads `iters` 16-byte
+ * vectors from it at consecutive addresses (no bank conflicts), so the
+ * launch reads blocks * threads * iters * 16 bytes of LDS.  d_sink: device
+ * uint32 [8]; workgroup 0's thread 0 writes the shader-clock ticks (sink[2],
+ * sink[3]: low, high word) and the constant-rate wall-clock ticks (sink[4],
+ * sink[5]) it measured around its read loop; the caller times the launch
+ * with events on the same stream.  Returns EPIC_ERR_ARG for sizes out of
+ * range. */
+epic_status epic_diag_lds_stream(int32_t blocks, int32_t threads, int32_t iters, uint32_t* d_sink,
+                                 hipStream_t stream);
+
+/* Shader-clock and wall-clock rates of the current device in kHz (as the
+ * runtime reports them), for epic_diag_lds_stream's tick counts. */
+epic_status epic_diag_clock_rates(int32_t* shader_khz, int32_t* wall_khz);
+
 const char* epic_status_string(epic_status s);
 
 #ifdef __cplusplus

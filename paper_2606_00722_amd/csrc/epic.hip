@@ -503,9 +503,13 @@ EPIC_INLINE int select_walk_body(const DevTab& tb, Lds<W>& L, const WgWork& wk, 
   }
 }
 
-// A check walk kept as a function of its own for 16-word item sets: at 1024
-// threads per workgroup (128 registers per lane) it measured faster than the
-// inlined walk, which spills in its inner loops; narrower item sets inline it.
+// A check walk kept as a function of its own for 16-word item sets in the
+// selection: at 1024 threads per workgroup (128 registers per lane) it
+// measured faster than the inlined walk, which spills in its inner loops
+// (C-like selection 29.9 against 31.7 ms per 256-token step, 4.27 against
+// 4.34 ms per 1024-token step), although the call frame costs more per-lane
+// scratch.  Narrower item sets, and the sequential fallback (512 threads,
+// where the inlined walk needs no scratch), inline it.
 template <int W, bool COVER, bool SHARE>
 __device__ __attribute__((noinline)) int select_walk_call(const DevTab& tb, Lds<W>& L, const WgWork& wk,
                                                           const WsArgs& ws, const int32_t* __restrict__ seqs, int n,
@@ -513,10 +517,10 @@ __device__ __attribute__((noinline)) int select_walk_call(const DevTab& tb, Lds<
   return select_walk_body<W, COVER, SHARE>(tb, L, wk, ws, seqs, n, b, msk);
 }
 
-template <int W, bool COVER, bool SHARE>
+template <int W, bool COVER, bool SHARE, bool CALL = (W >= 16)>
 EPIC_INLINE int select_walk(const DevTab& tb, Lds<W>& L, const WgWork& wk, const WsArgs& ws,
                                   const int32_t* __restrict__ seqs, int n, int b, uint64_t msk) {
-  if constexpr (W >= 16)
+  if constexpr (CALL)
     return select_walk_call<W, COVER, SHARE>(tb, L, wk, ws, seqs, n, b, msk);
   else
     return select_walk_body<W, COVER, SHARE>(tb, L, wk, ws, seqs, n, b, msk);
@@ -769,8 +773,9 @@ __global__ void __launch_bounds__(NT) select_kernel(DevTab tb, const int32_t* __
 // verdict-1 candidates are walked: filling masked positions only shrinks the
 // character language of x (a masked run reads any bytes), so a candidate
 // invalid on x stays invalid on every later x.  One workgroup per sequence;
-// the checks are the selection's exact walks.
-template <int W, int NT>
+// the checks are the selection's exact walks (with SHARE, resumed from the
+// sequence's base walk at the masked run of the lowest committed position).
+template <int W, int NT, bool SHARE>
 __global__ void __launch_bounds__(NT) fallback_kernel(DevTab tb, const int32_t* __restrict__ seqs, int B, int n,
                                                       const int32_t* __restrict__ cseq,
                                                       const int32_t* __restrict__ cpos,
@@ -803,7 +808,7 @@ __global__ void __launch_bounds__(NT) fallback_kernel(DevTab tb, const int32_t* 
     if (!L.sel_bad) {
       for (int i = 0; i < L.sel_n && need > 0; ++i) {
         if ((kept >> i) & 1) continue;
-        const int r = select_walk<W, false, false>(tb, L, wk, ws, seqs, n, b, kept | (1ull << i));
+        const int r = select_walk<W, false, SHARE, false>(tb, L, wk, ws, seqs, n, b, kept | (1ull << i));
         if (r < 0) {
           if (threadIdx.x == 0)
             atomicOr(tb.dev_err, (uint32_t)EPIC_DEV_CAPACITY | (1u << (8 + (L.overflow & 15))));
@@ -849,7 +854,6 @@ struct epic_ctx {
   int base_slots = 0;
   size_t off_snap = 0, snap_bytes = 0, off_spec = 0, off_bseq = 0;
   uint64_t tag = 0;  // owner tag of the base records this context writes
-  bool cover_bases = false;  // the last base launch also walked the cover graphs
   void* scratch = nullptr;  // this device's static scratch (epic_validate_batch_noalloc)
   // diagnostics: per-kernel HIP-event timing (epic_ctx_set_timing)
   bool timing = false;
@@ -1124,9 +1128,18 @@ epic_status FallbackLaunch<W>::run(epic_ctx* c, const int32_t* seqs, int B, int 
                                    const uint8_t* sel, const int32_t* num_commit, int C, uint8_t* accepted,
                                    void* ws, hipStream_t stream) {
   const int grid = std::min(B, c->nslot);
+  const WsArgs wa = ws_args(c, ws);
+  // long sequences: the loop's exact checks resume from the base walks of the
+  // Earley graphs, as the selection's do
+  const bool share = n >= kShareSelectLen && B <= c->base_slots;
+  if (share) launch_base<W>(c, seqs, B, n, B, wa, stream);
   KernelTimer kt(c, kKFallback, stream);
-  hipLaunchKernelGGL((fallback_kernel<W, kThreads>), dim3(grid), dim3(kThreads), 0, stream, tab_for(c, kKFallback),
-                     seqs, B, n, cs, cp, ct, conf, verdict, sel, num_commit, C, accepted, ws_args(c, ws));
+  if (share)
+    hipLaunchKernelGGL((fallback_kernel<W, kThreads, true>), dim3(grid), dim3(kThreads), 0, stream,
+                       tab_for(c, kKFallback), seqs, B, n, cs, cp, ct, conf, verdict, sel, num_commit, C, accepted, wa);
+  else
+    hipLaunchKernelGGL((fallback_kernel<W, kThreads, false>), dim3(grid), dim3(kThreads), 0, stream,
+                       tab_for(c, kKFallback), seqs, B, n, cs, cp, ct, conf, verdict, sel, num_commit, C, accepted, wa);
   return hipGetLastError() == hipSuccess ? EPIC_OK : EPIC_ERR_HIP;
 }
 
@@ -1196,6 +1209,39 @@ epic_status dispatch_w(int W, Args... args) {
   }
 }
 
+// LDS streaming microbenchmark (epic_diag_lds_stream): 64 KiB of LDS read
+// as 16-byte vectors at consecutive addresses per wavefront.  The stride and
+// the index mask are kernel arguments, so no two reads of the loop are known
+// to the compiler to hit the same address (none is merged away).
+__global__ void __launch_bounds__(1024) lds_stream_kernel(int iters, int stride, int mask,
+                                                          uint32_t* __restrict__ sink) {
+  __shared__ uint4 buf[4096];
+  const int t = (int)threadIdx.x, nt = (int)blockDim.x;
+  for (int i = t; i < 4096; i += nt) buf[i] = make_uint4((uint32_t)i, 3u * i, 5u * i, 7u * i);
+  __syncthreads();
+  const long long c0 = (long long)clock64(), w0 = (long long)wall_clock64();
+  uint32_t a0 = 0, a1 = 0, a2 = 0, a3 = 0;
+  int idx = t;
+#pragma unroll 8
+  for (int k = 0; k < iters; ++k) {
+    const uint4 v = buf[idx & mask];
+    a0 += v.x;
+    a1 += v.y;
+    a2 += v.z;
+    a3 += v.w;
+    idx += stride;
+  }
+  const long long c1 = (long long)clock64(), w1 = (long long)wall_clock64();
+  if ((a0 ^ a1 ^ a2 ^ a3) == 0x9E3779B9u) sink[0] = 1u;  // keeps the reads
+  if (blockIdx.x == 0 && t == 0) {
+    const unsigned long long dc = (unsigned long long)(c1 - c0), dw = (unsigned long long)(w1 - w0);
+    sink[2] = (uint32_t)dc;
+    sink[3] = (uint32_t)(dc >> 32);
+    sink[4] = (uint32_t)dw;
+    sink[5] = (uint32_t)(dw >> 32);
+  }
+}
+
 extern "C" {
 
 static epic_status read_counters(epic_ctx* c, hipStream_t stream, int64_t* sets) {
@@ -1247,6 +1293,24 @@ epic_status epic_ctx_kernel_stats(epic_ctx* c, hipStream_t stream, double* ms, i
     c->kernel_launches[k] = 0;
     for (int i = 0; i < kWorkCounters; ++i) work[k * kWorkCounters + i] = sets[k * 8 + i];
   }
+  return EPIC_OK;
+}
+
+epic_status epic_diag_lds_stream(int32_t blocks, int32_t threads, int32_t iters, uint32_t* d_sink,
+                                 hipStream_t stream) {
+  if (!d_sink) return EPIC_ERR_NULL;
+  if (blocks < 1 || blocks > (1 << 20) || threads < 64 || threads > 1024 || threads % 64 != 0 || iters < 1)
+    return EPIC_ERR_ARG;
+  hipLaunchKernelGGL(lds_stream_kernel, dim3(blocks), dim3(threads), 0, stream, (int)iters, (int)threads, 4095, d_sink);
+  return hipGetLastError() == hipSuccess ? EPIC_OK : EPIC_ERR_HIP;
+}
+
+epic_status epic_diag_clock_rates(int32_t* shader_khz, int32_t* wall_khz) {
+  if (!shader_khz || !wall_khz) return EPIC_ERR_NULL;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return EPIC_ERR_HIP;
+  if (hipDeviceGetAttribute(shader_khz, hipDeviceAttributeClockRate, dev) != hipSuccess) return EPIC_ERR_HIP;
+  if (hipDeviceGetAttribute(wall_khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess) return EPIC_ERR_HIP;
   return EPIC_OK;
 }
 

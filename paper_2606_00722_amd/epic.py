@@ -27,7 +27,7 @@ FUNCTIONS = ["epic_ctx_create", "epic_ctx_destroy", "epic_workspace_bytes", "epi
              "epic_select_compatible",
              "epic_commit_fallback",
              "epic_ctx_device_error", "epic_ctx_work_counters", "epic_ctx_set_timing", "epic_ctx_kernel_stats",
-             "epic_status_string"]
+             "epic_diag_lds_stream", "epic_diag_clock_rates", "epic_status_string"]
 KERNEL_KINDS = ["lexmemo", "base", "validate", "select", "fallback", "spec_clear"]
 
 
@@ -91,6 +91,10 @@ def lib() -> ctypes.CDLL:
         L.epic_ctx_set_timing.restype = ctypes.c_int
         L.epic_ctx_kernel_stats.argtypes = [P, P, P, P, P]
         L.epic_ctx_kernel_stats.restype = ctypes.c_int
+        L.epic_diag_lds_stream.argtypes = [i32, i32, i32, P, P]
+        L.epic_diag_lds_stream.restype = ctypes.c_int
+        L.epic_diag_clock_rates.argtypes = [ctypes.POINTER(i32), ctypes.POINTER(i32)]
+        L.epic_diag_clock_rates.restype = ctypes.c_int
         L.epic_status_string.argtypes = [ctypes.c_int]
         L.epic_status_string.restype = ctypes.c_char_p
         _lib = L
@@ -241,3 +245,17 @@ class Context:
         f = ctypes.c_uint32(0)
         _check("epic_ctx_device_error", lib().epic_ctx_device_error(self._h, _stream(stream), ctypes.byref(f)))
         return int(f.value)
+
+
+def lds_stream(blocks: int, threads: int, iters: int, sink, stream=None):
+    """Launch the LDS streaming microbenchmark (epic_diag_lds_stream) on a
+    torch uint32 device tensor of 8 elements."""
+    _check("epic_diag_lds_stream", lib().epic_diag_lds_stream(int(blocks), int(threads), int(iters), _ptr(sink),
+                                                               _stream(stream)))
+
+
+def clock_rates() -> tuple:
+    """(shader clock kHz, wall clock kHz) of the current device."""
+    a, b = ctypes.c_int32(0), ctypes.c_int32(0)
+    _check("epic_diag_clock_rates", lib().epic_diag_clock_rates(ctypes.byref(a), ctypes.byref(b)))
+    return int(a.value), int(b.value)

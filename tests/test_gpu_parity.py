@@ -153,14 +153,16 @@ def test_padded_grammar_item_widths(preset, words, gpu_mod, oracle_lib):
 
 
 @pytest.mark.parametrize("batch", ["alg4", "empty"])
-@pytest.mark.parametrize("preset,B", [(1, None), (2, None), (3, 6), (4, 1)])
+@pytest.mark.parametrize("preset,B", [(1, None), (2, None), (3, 6), (4, 1), (5, 4)])
 def test_commit_fallback_matches_oracle(preset, B, batch, gpu_mod, oracle_lib):
     """The sequential fallback after the relaxed batch, with the oracle's
     verdicts as input and a seeded commit budget per sequence; the batch is
     Alg. 4's selection, or empty (the case where the loop decides every
     commit, accepting and rejecting candidates against the updated x).  The
     candidates the device commits equal the oracle's, which checks every
-    candidate it reaches (the device walks verdict-1 ones only)."""
+    candidate it reaches (the device walks verdict-1 ones only).  The
+    1024-token workload takes the launch whose checks resume from the base
+    walks of the sequences."""
     import torch
 
     inst = W.make_instance(preset, 42, B=B)
