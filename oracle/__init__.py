@@ -63,6 +63,7 @@ def lib() -> ctypes.CDLL:
         L.oracle_dfa_states.argtypes = [P, P, P, P, i32]
         L.oracle_validate_batch.argtypes = [P, P, P, P, i32, i32, P, P, P, i32, P, i32]
         L.oracle_select.argtypes = [P, P, P, P, i32, i32, P, P, P, P, P, i32, P, P, i32]
+        L.oracle_witness.argtypes = [P, P, P, P, i32, P, i32, P, i32, P]
         _lib = L
     return _lib
 
@@ -168,6 +169,27 @@ def dfa_states(p: Problem, x) -> int:
     xs = _seq(x)
     lx, gr, vc = p.refs
     return lib().oracle_dfa_states(lx, gr, vc, _ptr(xs) if xs.size else _ptr(np.zeros(1, np.int32)), int(xs.size))
+
+
+def witness(p: Problem, x):
+    """A completion of x (failure recovery, Sec. 4): (1, [bytes of each
+    maximal masked run, in order]) when x is valid, (0, None) when it is not,
+    (-3, None) on a construction limit of the oracle."""
+    xs = _seq(x)
+    lx, gr, vc = p.refs
+    cap, max_gaps = 1 << 16, max(1, int(xs.size))
+    out = np.zeros(cap, dtype=np.uint8)
+    lens = np.zeros(max_gaps, dtype=np.int32)
+    ng = ctypes.c_int32(0)
+    r = lib().oracle_witness(lx, gr, vc, _ptr(xs) if xs.size else _ptr(np.zeros(1, np.int32)), int(xs.size),
+                             _ptr(out), cap, _ptr(lens), max_gaps, ctypes.byref(ng))
+    if r != 1:
+        return r, None
+    gaps, k = [], 0
+    for j in range(ng.value):
+        gaps.append(bytes(out[k:k + lens[j]]))
+        k += int(lens[j])
+    return 1, gaps
 
 
 def _cands(seq, pos, tok):

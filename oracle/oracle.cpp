@@ -31,6 +31,12 @@
 //    of G (App. A.2, App. D.3 "Regular Cover"): entry/exit states per
 //    nonterminal, one state per rule position, every call site flattened.
 //    Decided by breadth-first search of the product with the same DFA.
+//  * Witness (Sec. 4, failure recovery: a valid x has a completion, and the
+//    output is completed from it): the Bar-Hillel triples of the same DFA
+//    (App. A.2), found in rounds so that the expansion of (S, start, final)
+//    terminates, give a terminal string of L(G) accepted by A_x; a breadth-first
+//    search of A_x finds a path spelling it; its moves inside masked runs give
+//    the bytes of each run.
 //  * Select: Alg. 4 (RelaxedSelect then ExactShrink) over the candidates of a
 //    sequence whose individual verdict is 1, sorted by descending float32
 //    confidence with ties to the lower candidate index, halves split with the
@@ -501,6 +507,170 @@ int relaxed_seq(const Lexer& L, const Grammar& G, const Vocab& V, const std::vec
   return cover_accepts(build_cover(G), D) ? 1 : 0;
 }
 
+// ----- witness: a completion of x (Sec. 4, failure recovery) ---------------------
+// Bar-Hillel triples (B, p, q) of a terminal DFA D: nonterminal B derives a
+// terminal string that takes D from state p to state q (the intersection
+// construction behind the completable criterion, App. A.2).  Found in rounds:
+// a triple found in round r keeps its production and the DFA states between
+// its symbols, built from terminal moves and triples of rounds before r only,
+// so that expanding a triple into a string terminates.
+struct Triples {
+  struct Rec {
+    int round, prod;
+    std::vector<int> states;  // |rhs| + 1 states, first = p, last = q
+  };
+  int N = 0, D = 0;
+  std::unordered_map<uint64_t, Rec> rec;
+  std::vector<std::vector<std::pair<int, int>>> out;  // [B * D + p]: (q, round)
+  uint64_t key(int B, int p, int q) const { return ((uint64_t)B * D + p) * D + q; }
+  const Rec* find(int B, int p, int q) const {
+    auto it = rec.find(key(B, p, q));
+    return it == rec.end() ? nullptr : &it->second;
+  }
+};
+
+// returns false when D has more than `limit` states
+bool bar_hillel_triples(const GrammarView& g, const DFA& D, Triples& T, int limit) {
+  T = Triples();
+  T.N = g.N;
+  T.D = D.states();
+  if (T.D > limit) return false;
+  T.out.assign((size_t)g.N * T.D, {});
+  for (int round = 1;; ++round) {
+    std::vector<std::pair<uint64_t, Triples::Rec>> found;
+    for (int pr = 0; pr < g.P; ++pr) {
+      const int B = g.lhs[pr] - g.T;
+      const auto& r = g.rhs[pr];
+      for (int p = 0; p < T.D; ++p) {
+        // layer[i]: state after i symbols -> state after i - 1 symbols
+        std::vector<std::map<int, int>> layer(r.size() + 1);
+        layer[0][p] = -1;
+        for (size_t i = 0; i < r.size(); ++i) {
+          const int X = r[i];
+          for (auto& kv : layer[i]) {
+            const int st = kv.first;
+            if (X < g.T) {
+              const int nx = D.trans[st][X];
+              if (nx >= 0 && !layer[i + 1].count(nx)) layer[i + 1][nx] = st;
+            } else {
+              for (auto& qr : T.out[(size_t)(X - g.T) * T.D + st])
+                if (qr.second < round && !layer[i + 1].count(qr.first)) layer[i + 1][qr.first] = st;
+            }
+          }
+          if (layer[i + 1].empty()) break;
+        }
+        for (auto& kv : layer[r.size()]) {
+          const int q = kv.first;
+          if (T.rec.count(T.key(B, p, q))) continue;
+          Triples::Rec rc{round, pr, std::vector<int>(r.size() + 1)};
+          int st = q;
+          for (size_t i = r.size(); i > 0; --i) {
+            rc.states[i] = st;
+            st = layer[i][st];
+          }
+          rc.states[0] = p;
+          found.push_back({T.key(B, p, q), rc});
+        }
+      }
+    }
+    int added = 0;
+    for (auto& f : found) {
+      if (T.rec.count(f.first)) continue;  // the same triple from two productions in one round
+      const int B = (int)(f.first / ((uint64_t)T.D * T.D)), p = (int)(f.first / T.D % T.D), q = (int)(f.first % T.D);
+      T.out[(size_t)B * T.D + p].push_back({q, round});
+      T.rec.emplace(f.first, std::move(f.second));
+      ++added;
+    }
+    if (!added) break;
+  }
+  return true;
+}
+
+// The terminal string of triple (B, p, q), appended to w.
+void expand_triple(const GrammarView& g, const Triples& T, int B, int p, int q, std::vector<int>& w) {
+  const Triples::Rec* rc = T.find(B, p, q);
+  const auto& r = g.rhs[rc->prod];
+  for (size_t i = 0; i < r.size(); ++i) {
+    if (r[i] < g.T)
+      w.push_back(r[i]);
+    else
+      expand_triple(g, T, r[i] - g.T, rc->states[i], rc->states[i + 1], w);
+  }
+}
+
+// Witness of x: 1 with the bytes of every maximal masked run (in order) in
+// gaps, 0 when x is not valid, -3 when a construction limit is exceeded.
+int witness_seq(const Lexer& L, const Grammar& G, const Vocab& V, const std::vector<int32_t>& x,
+                std::vector<std::vector<uint8_t>>& gaps) {
+  gaps.clear();
+  const std::vector<int> slots = make_slots(V, x.data(), (int)x.size());
+  CharNFA A;
+  build_char_nfa(L, slots, A);
+  DFA D;
+  if (!determinize(A, G.T, D, 4000000)) return -3;
+  if (D.start < 0) return 0;
+  minimize(D);
+  GrammarView g(G);
+  Triples T;
+  if (!bar_hillel_triples(g, D, T, 20000)) return -3;
+  int fin = -1;
+  for (int f = 0; f < D.states() && fin < 0; ++f)
+    if (D.fin[f] && T.find(G.start - G.T, D.start, f)) fin = f;
+  if (fin < 0) return 0;
+  std::vector<int> w;
+  expand_triple(g, T, G.start - G.T, D.start, fin, w);
+  // a path of A_x spelling w: breadth-first over (node, symbols read)
+  const int nn = (int)A.alive.size(), m = (int)w.size();
+  auto id = [m](int u, int i) { return (int64_t)u * (m + 1) + i; };
+  std::unordered_map<int64_t, int64_t> pred;
+  std::deque<int64_t> queue;
+  const int64_t s0 = id(0, 0), goal = id(A.final_node, m);
+  pred[s0] = -1;
+  queue.push_back(s0);
+  while (!queue.empty() && !pred.count(goal)) {
+    const int64_t cur = queue.front();
+    queue.pop_front();
+    const int u = (int)(cur / (m + 1)), i = (int)(cur % (m + 1));
+    auto visit = [&](int v, int j) {
+      if (v < 0 || v >= nn || !A.alive[v]) return;
+      const int64_t nx = id(v, j);
+      if (pred.emplace(nx, cur).second) queue.push_back(nx);
+    };
+    for (int v : A.eps[u]) visit(v, i);
+    if (i < m)
+      for (auto& e : A.lab[u])
+        if (e.first == w[i]) visit(e.second, i + 1);
+  }
+  if (!pred.count(goal)) return -3;  // cannot happen: D and A_x have the same language
+  std::vector<int64_t> path;
+  for (int64_t c = goal; c >= 0; c = pred[c]) path.push_back(c);
+  std::reverse(path.begin(), path.end());
+  // bytes of the moves inside masked runs
+  std::vector<int> gap_of(slots.size() + 1, -1);
+  int ng = 0;
+  for (size_t k = 0; k < slots.size(); ++k)
+    if (slots[k] == -1) gap_of[k] = ng++;
+  gaps.assign(ng, {});
+  for (size_t k = 0; k + 1 < path.size(); ++k) {
+    const int u = (int)(path[k] / (m + 1)), v = (int)(path[k + 1] / (m + 1));
+    const bool labelled = path[k + 1] % (m + 1) != path[k] % (m + 1);
+    if (u == A.final_node || v == A.final_node) continue;
+    const int su = u / A.Q, qu = u % A.Q, sv = v / A.Q, qv = v % A.Q;
+    if (su >= A.S || slots[su] != -1 || sv != su) continue;  // fixed byte, or leaving the run
+    int byte = -1;
+    for (int c = 0; c < 256 && byte < 0; ++c) {
+      int o;
+      const int q2 = lex_step(L, qu, c, &o);
+      if (q2 != qv) continue;
+      const bool emits = o != kNone && o != kSkip;
+      if (labelled ? (emits && o == w[path[k] % (m + 1)]) : !emits) byte = c;
+    }
+    if (byte < 0) return -3;  // cannot happen: the move was made by some byte
+    gaps[gap_of[su]].push_back((uint8_t)byte);
+  }
+  return 1;
+}
+
 struct Cand {
   int idx, pos, tok;
   float conf;
@@ -683,6 +853,28 @@ int oracle_valid(const oracle_lexer* l, const oracle_grammar* g, const oracle_vo
 int oracle_cover(const oracle_lexer* l, const oracle_grammar* g, const oracle_vocab* v, const int32_t* x, int n) {
   std::vector<int32_t> xs(x, x + n);
   return relaxed_seq(to_lexer(l), to_grammar(g), to_vocab(v), xs);
+}
+
+// Witness of x (failure recovery, Sec. 4): returns 1 and writes the bytes of
+// each maximal masked run of x, in order, to out (gap_len[j] bytes for run j,
+// *num_gaps runs); 0 when x is not valid; -3 on a construction limit; -2 when
+// out or gap_len is too small.
+int oracle_witness(const oracle_lexer* l, const oracle_grammar* g, const oracle_vocab* v, const int32_t* x, int n,
+                   uint8_t* out, int cap, int32_t* gap_len, int max_gaps, int32_t* num_gaps) {
+  std::vector<int32_t> xs(x, x + n);
+  std::vector<std::vector<uint8_t>> gaps;
+  const int r = witness_seq(to_lexer(l), to_grammar(g), to_vocab(v), xs, gaps);
+  *num_gaps = (int32_t)gaps.size();
+  if (r != 1) return r;
+  if ((int)gaps.size() > max_gaps) return -2;
+  int k = 0;
+  for (size_t j = 0; j < gaps.size(); ++j) {
+    if (k + (int)gaps[j].size() > cap) return -2;
+    std::memcpy(out + k, gaps[j].data(), gaps[j].size());
+    gap_len[j] = (int32_t)gaps[j].size();
+    k += (int)gaps[j].size();
+  }
+  return 1;
 }
 
 // Number of states of the minimal completion DFA of x (diagnostics), -3 on blow-up.

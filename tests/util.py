@@ -69,3 +69,19 @@ def packed_words(g: G.Grammar) -> int:
     while w < len(bins):
         w *= 2
     return w
+
+
+def fill(vocab_strings, x, gaps) -> bytes:
+    """The bytes of x with its j-th maximal masked run replaced by gaps[j]."""
+    out, g, prev_masked = [], 0, False
+    for t in x:
+        if t < 0:
+            if not prev_masked:
+                out.append(gaps[g])
+                g += 1
+            prev_masked = True
+        else:
+            out.append(vocab_strings[int(t)])
+            prev_masked = False
+    assert g == len(gaps)
+    return b"".join(out)
