@@ -13,8 +13,10 @@ fallback (Alg. 1 in App. C.1; after the selected subset and after an empty
 one, seeded budgets) must be bit-exact.  Because each step's inputs follow
 from the previous step's outputs, a single differing bit anywhere stops the
 replay at that step."""
+import glob
 import json
 import os
+import re
 
 import numpy as np
 import pytest
@@ -24,7 +26,10 @@ from tests.golden import make_trajectories as MT
 
 pytestmark = pytest.mark.gpu
 
-CASES = [(p, s) for p in (1, 2) for s in (42, 43, 44)]
+# every stored trajectory (presets 1-5, seeds 42-44)
+CASES = sorted((int(m.group(1)), int(m.group(2))) for m in
+               (re.search(r"traj_p(\d)_s(\d+)\.jsonl$", f) for f in glob.glob(os.path.join(os.path.dirname(MT.__file__),
+                                                                                        "traj_p*_s*.jsonl"))) if m)
 
 
 @pytest.fixture(scope="module")
