@@ -253,6 +253,31 @@ epic_status epic_ctx_set_timing(epic_ctx* ctx, int32_t enable);
  * elements. */
 epic_status epic_ctx_kernel_stats(epic_ctx* ctx, hipStream_t stream, double* ms, int64_t* launches, int64_t* work);
 
+/* Witness extraction for failure recovery (Sec. 4): when decoding stops
+ * early, the output is completed from a witness of the current partial
+ * sequence, which is completable because every committed update was checked.
+ * For each sequence b of d_seqs (int32 [B*n], -1 = MASK), d_status[b]
+ * (int32) is 1 when x_b is valid and a completion was found, 0 when x_b is
+ * not valid, -1 when a token is out of range (EPIC_DEV_BAD_CANDIDATE), -2
+ * when a buffer is too small (the witness workspace, bytes_per_seq or
+ * max_gaps; EPIC_DEV_CAPACITY), -3 when no completion was found (not expected
+ * for a valid x_b).  With status 1, d_gap_len[b*max_gaps + j] (int32) is the
+ * number of bytes that fill the j-th maximal masked run of x_b, and
+ * d_bytes[b*bytes_per_seq ..] holds the bytes of the runs in order: x_b with
+ * every run replaced by its bytes lexes into a sentence of L(G).  A masked
+ * run reads any byte string (the paper's over-approximation of masked
+ * regions), so a filling is a byte string, not a number of tokens.
+ * d_witness_ws: device memory of epic_witness_workspace_bytes(ctx, B) bytes,
+ * 256-byte aligned, owned by the caller; d_workspace is the context's
+ * workspace (its chart slots hold the walks).  B may not exceed the walk
+ * slots of the context (min(max(max_cands, max_batch), 1024)):
+ * EPIC_ERR_CAPACITY.  Asynchronous on stream. */
+size_t epic_witness_workspace_bytes(const epic_ctx* ctx, int32_t B);
+epic_status epic_witness(epic_ctx* ctx, const int32_t* d_seqs, int32_t B, int32_t n, uint8_t* d_bytes,
+                         int32_t bytes_per_seq, int32_t* d_gap_len, int32_t max_gaps, int32_t* d_status,
+                         void* d_witness_ws, size_t witness_ws_bytes, void* d_workspace, size_t workspace_bytes,
+                         hipStream_t stream);
+
 /* Diagnostics: LDS streaming microbenchmark, the measurement behind the LDS
  * peak that walk kernels are compared with.  Launches `blocks` workgroups of
  * `threads` threads (a multiple of 64, at most 1024) on `stream`; each

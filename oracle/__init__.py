@@ -64,6 +64,7 @@ def lib() -> ctypes.CDLL:
         L.oracle_validate_batch.argtypes = [P, P, P, P, i32, i32, P, P, P, i32, P, i32]
         L.oracle_select.argtypes = [P, P, P, P, i32, i32, P, P, P, P, P, i32, P, P, i32]
         L.oracle_witness.argtypes = [P, P, P, P, i32, P, i32, P, i32, P]
+        L.oracle_valid_text.argtypes = [P, P, P, i32]
         _lib = L
     return _lib
 
@@ -190,6 +191,14 @@ def witness(p: Problem, x):
         gaps.append(bytes(out[k:k + lens[j]]))
         k += int(lens[j])
     return 1, gaps
+
+
+def valid_text(p: Problem, text: bytes) -> int:
+    """Valid of a byte string with no masks (greedy lexing, then membership in
+    L(G)): 1, 0, or -3 on a construction limit."""
+    buf = np.frombuffer(text, dtype=np.uint8).copy() if text else np.zeros(1, np.uint8)
+    lx, gr, _ = p.refs
+    return lib().oracle_valid_text(lx, gr, _ptr(buf), len(text))
 
 
 def _cands(seq, pos, tok):

@@ -877,6 +877,19 @@ int oracle_witness(const oracle_lexer* l, const oracle_grammar* g, const oracle_
   return 1;
 }
 
+// Valid of a byte string with no masks: 1 when its greedy lexing is defined
+// and in L(G) (Sec. 3 with M(x) empty), 0 otherwise, -3 on a limit.
+int oracle_valid_text(const oracle_lexer* l, const oracle_grammar* g, const uint8_t* text, int len) {
+  std::vector<int> slots(text, text + len);
+  CharNFA A;
+  build_char_nfa(to_lexer(l), slots, A);
+  DFA D;
+  if (!determinize(A, g->num_terminals, D, 4000000)) return -3;
+  if (D.start >= 0) minimize(D);
+  GrammarView gv(to_grammar(g));
+  return earley_accepts(gv, D) ? 1 : 0;
+}
+
 // Number of states of the minimal completion DFA of x (diagnostics), -3 on blow-up.
 int oracle_dfa_states(const oracle_lexer* l, const oracle_grammar* g, const oracle_vocab* v, const int32_t* x, int n) {
   DFA D;

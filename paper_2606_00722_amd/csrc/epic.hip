@@ -159,6 +159,7 @@ __device__ inline WgWork slot_work(const WsArgs& a, int slot) {
   w.b_cov = w.cov;
   w.split_node = 0;
   w.split_ent = 0;
+  w.rec = nullptr;
   return w;
 }
 __device__ inline char* snap_record(const WsArgs& a, int b) { return a.base + a.snap_off + (size_t)b * a.snap_bytes; }
@@ -826,6 +827,8 @@ __global__ void __launch_bounds__(NT) fallback_kernel(DevTab tb, const int32_t* 
   }
 }
 
+#include "witness.inc"
+
 }  // namespace epic
 
 // ==================================================================== C ABI
@@ -855,6 +858,10 @@ struct epic_ctx {
   size_t off_snap = 0, snap_bytes = 0, off_spec = 0, off_bseq = 0;
   uint64_t tag = 0;  // owner tag of the base records this context writes
   void* scratch = nullptr;  // this device's static scratch (epic_validate_batch_noalloc)
+  // witness workspace layout, per sequence (epic_witness)
+  size_t wit_stride = 0, wit_rec = 0, wit_mark = 0, wit_stack = 0, wit_w = 0, wit_recs = 0, wit_vis = 0;
+  size_t wit_proof = 0, wit_pindex = 0, wit_sys = 0;
+  int wit_ecap = 0;
   // diagnostics: per-kernel HIP-event timing (epic_ctx_set_timing)
   bool timing = false;
   struct Pending {
@@ -889,7 +896,9 @@ epic_status upload(epic_ctx* c) {
          o_gtm = place(blob, H.gap_tm), o_gown = place(blob, H.gap_own), o_ccl = place(blob, H.cover_cl),
          o_enib = place(blob, H.expn_nib), o_pnib = place(blob, H.pred_nib), o_gcov = place(blob, H.gap_cover),
          o_lnib = place(blob, H.lhs_nib), o_snib = place(blob, H.sym_nib),
-         o_vb = place(blob, H.vbytes), o_vo = place(blob, H.voffs);
+         o_vb = place(blob, H.vbytes), o_vo = place(blob, H.voffs), o_endof = place(blob, H.end_of),
+         o_dot0 = place(blob, H.dot0), o_wynt = place(blob, H.wy_nt), o_wyown = place(blob, H.wy_own),
+         o_wypool = place(blob, H.wy_pool);
   {
     // owner tag of the walk records this context writes: FNV-1a over every
     // constant table (the memo is a function of them) and the workspace
@@ -955,6 +964,12 @@ epic_status upload(epic_ctx* c) {
   t.cover_cl = (const uint32_t*)(d + o_ccl);
   t.vbytes = (const uint8_t*)(d + o_vb);
   t.voffs = (const int32_t*)(d + o_vo);
+  t.end_of = (const uint32_t*)(d + o_endof);
+  t.dot0 = (const uint32_t*)(d + o_dot0);
+  t.nullable = H.nullable;
+  t.wy_nt = (const int32_t*)(d + o_wynt);
+  t.wy_own = (const int32_t*)(d + o_wyown);
+  t.wy_pool = (const uint8_t*)(d + o_wypool);
   t.memo = c->d_memo;
   t.dev_err = c->d_err;
   t.work = (unsigned long long*)((char*)c->d_err + kWorkOff);
@@ -979,6 +994,40 @@ WsArgs ws_args(const epic_ctx* c, void* ws) {
   a.bseq_off = c->off_bseq;
   a.snap_off = c->off_snap;
   a.snap_bytes = c->snap_bytes;
+  return a;
+}
+
+constexpr int kWitFrames = 1 << 15;    // back-trace stack
+constexpr int kWitTerminals = 1 << 15; // terminals of a witness
+constexpr int kWitRecords = 1 << 20;   // byte-search records
+constexpr int kWitProofs = 1 << 18;    // stored proofs of the back-trace
+constexpr int kWitProofSlots = 1 << 19;
+constexpr int kWitSystems = 1 << 12;   // masked-run systems ranked by the back-trace
+constexpr int kWitVisWords = 1 << 15;  // byte-search visited set (bits: lexer states x window)
+constexpr int kWitSteps = 1 << 22;     // back-trace steps
+
+WitArgs wit_args(const epic_ctx* c, void* wws) {
+  WitArgs a;
+  a.base = (char*)wws;
+  a.stride = c->wit_stride;
+  a.off_rec = c->wit_rec;
+  a.off_mark = c->wit_mark;
+  a.off_stack = c->wit_stack;
+  a.off_w = c->wit_w;
+  a.off_recs = c->wit_recs;
+  a.off_vis = c->wit_vis;
+  a.off_proof = c->wit_proof;
+  a.off_pindex = c->wit_pindex;
+  a.off_sys = c->wit_sys;
+  a.syscap = kWitSystems;
+  a.pcap = kWitProofs;
+  a.pslots = kWitProofSlots;
+  a.ecap = c->wit_ecap;
+  a.scap = kWitFrames;
+  a.wcap = kWitTerminals;
+  a.rcap = kWitRecords;
+  a.vwords = kWitVisWords;
+  a.steps = kWitSteps;
   return a;
 }
 
@@ -1042,6 +1091,12 @@ struct FallbackLaunch {
   static epic_status run(epic_ctx* c, const int32_t* seqs, int B, int n, const int32_t* cs, const int32_t* cp,
                          const int32_t* ct, const float* conf, const uint8_t* verdict, const uint8_t* sel,
                          const int32_t* num_commit, int C, uint8_t* accepted, void* ws, hipStream_t stream);
+};
+
+template <int W>
+struct WitnessLaunch {
+  static epic_status run(epic_ctx* c, const int32_t* seqs, int B, int n, uint8_t* bytes, int bytes_per_seq,
+                         int32_t* gap_len, int max_gaps, int32_t* status, void* wws, void* ws, hipStream_t stream);
 };
 
 #ifdef EPIC_KERNEL_UNIT
@@ -1161,6 +1216,23 @@ epic_status ValidatePlainLaunch<W>::run(epic_ctx* c, const int32_t* seqs, int B,
   return hipGetLastError() == hipSuccess ? EPIC_OK : EPIC_ERR_HIP;
 }
 
+// Witness extraction: the recording walk of each sequence in chart slot b,
+// the back-trace (one wavefront per sequence), the byte search.
+template <int W>
+epic_status WitnessLaunch<W>::run(epic_ctx* c, const int32_t* seqs, int B, int n, uint8_t* bytes, int bytes_per_seq,
+                                  int32_t* gap_len, int max_gaps, int32_t* status, void* wws, void* ws,
+                                  hipStream_t stream) {
+  const WsArgs wa = ws_args(c, ws);
+  const WitArgs wt = wit_args(c, wws);
+  hipLaunchKernelGGL((witness_walk_kernel<W, kThreads>), dim3(B), dim3(kThreads), 0, stream, c->tab, seqs, B, n, wa,
+                     wt, status);
+  hipLaunchKernelGGL((witness_trace_kernel<W>), dim3(B), dim3(64), 0, stream, c->tab, wa, wt, status, B);
+  hipLaunchKernelGGL((witness_realize_kernel<256>), dim3(B), dim3(256), 0, stream, c->tab, seqs, B, n, wt, status,
+                     bytes, bytes_per_seq, gap_len, max_gaps);
+  return hipGetLastError() == hipSuccess ? EPIC_OK : EPIC_ERR_HIP;
+}
+
+template struct WitnessLaunch<EPIC_KERNEL_UNIT>;
 template struct ValidatePlainLaunch<EPIC_KERNEL_UNIT>;
 template struct ValidateLaunch<EPIC_KERNEL_UNIT>;
 template struct FallbackLaunch<EPIC_KERNEL_UNIT>;
@@ -1375,6 +1447,21 @@ epic_status epic_ctx_create(const epic_lexer_desc* lexer, const epic_grammar_des
   c->off_bseq = c->off_snap + c->snap_bytes * 2 * c->base_slots;
   c->off_spec = c->off_bseq + align256((size_t)2 * c->base_slots * max_seq_len * 4);
   c->ws_bytes = c->off_spec + align256((size_t)c->max_batch * kSpec * 8);  // + speculated checks
+  // witness workspace, per sequence: edge record, on-path marks (one bit per
+  // chart item), search stack, witness terminals, byte-search records and
+  // visited set, stored proofs and their index
+  c->wit_ecap = 4 * c->maxn + 4096;
+  c->wit_rec = 0;
+  c->wit_mark = align256((size_t)4 * (kRecHeader + 4 * (size_t)c->maxn + 4 * (size_t)c->wit_ecap));
+  c->wit_stack = c->wit_mark + align256((size_t)c->maxe * H.W * 4);
+  c->wit_w = c->wit_stack + align256((size_t)kWitFrames * sizeof(WitFrame));
+  c->wit_recs = c->wit_w + align256((size_t)(kWitTerminals + 1) * 4);
+  c->wit_vis = c->wit_recs + align256((size_t)kWitRecords * sizeof(WitRec));
+  c->wit_proof = c->wit_vis + align256((size_t)kWitVisWords * 4);
+  c->wit_pindex = c->wit_proof + align256((size_t)kWitProofs * sizeof(WitProof));
+  c->wit_sys = c->wit_pindex + align256((size_t)kWitProofSlots * 4);
+  c->wit_stride = c->wit_sys + align256((size_t)kWitSystems * 8 + (size_t)2 * kWitSystems * 4 + 256 * 4 +
+                                        (size_t)kWitSystems * std::max(H.K, 1) * H.NI * 2);
   epic_status s = upload(c);
   if (s != EPIC_OK) {
     epic_ctx_destroy(c);
@@ -1491,6 +1578,26 @@ epic_status epic_commit_fallback(epic_ctx* c, const int32_t* d_seqs, int32_t B, 
   if (!d_conf || !d_verdict || !d_selected || !d_num_commit) return EPIC_ERR_NULL;
   return dispatch_w<FallbackLaunch>(c->H.W, c, d_seqs, (int)B, (int)n, d_cand_seq, d_cand_pos, d_cand_tok, d_conf,
                                     d_verdict, d_selected, d_num_commit, (int)C, d_accepted, d_workspace, stream);
+}
+
+size_t epic_witness_workspace_bytes(const epic_ctx* c, int32_t B) {
+  return c && B > 0 ? c->wit_stride * (size_t)B : 0;
+}
+
+epic_status epic_witness(epic_ctx* c, const int32_t* d_seqs, int32_t B, int32_t n, uint8_t* d_bytes,
+                         int32_t bytes_per_seq, int32_t* d_gap_len, int32_t max_gaps, int32_t* d_status,
+                         void* d_witness_ws, size_t witness_ws_bytes, void* d_workspace, size_t workspace_bytes,
+                         hipStream_t stream) {
+  if (!c) return EPIC_ERR_NULL;
+  if (B < 0 || n < 1 || bytes_per_seq < 0 || max_gaps < 1) return EPIC_ERR_ARG;
+  if (B > c->max_batch || B > c->nslot || n > c->max_seq) return EPIC_ERR_CAPACITY;
+  if (B == 0) return EPIC_OK;
+  if (!d_seqs || !d_bytes || !d_gap_len || !d_status || !d_witness_ws || !d_workspace) return EPIC_ERR_NULL;
+  if (((uintptr_t)d_workspace & 255) != 0 || ((uintptr_t)d_witness_ws & 255) != 0) return EPIC_ERR_ARG;
+  if (workspace_bytes < c->ws_bytes || witness_ws_bytes < c->wit_stride * (size_t)B) return EPIC_ERR_CAPACITY;
+  if (!c->memo_built) return EPIC_ERR_STATE;
+  return dispatch_w<WitnessLaunch>(c->H.W, c, d_seqs, (int)B, (int)n, d_bytes, (int)bytes_per_seq, d_gap_len,
+                                   (int)max_gaps, d_status, d_witness_ws, d_workspace, stream);
 }
 
 epic_status epic_ctx_device_error(epic_ctx* c, hipStream_t stream, uint32_t* flags) {

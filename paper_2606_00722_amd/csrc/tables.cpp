@@ -23,6 +23,7 @@
 #include "tables.h"
 
 #include <algorithm>
+#include <functional>
 #include <map>
 #include <set>
 #include <vector>
@@ -47,6 +48,174 @@ struct Bits {
 };
 
 inline void set32(std::vector<uint32_t>& v, size_t base, int i) { v[base + (i >> 5)] |= 1u << (i & 31); }
+
+// Terminal strings of the derivations inside a masked run (witness
+// extraction).  Nonterminal derivations between classes are found in rounds
+// (a derivation found in round r uses terminal edges, epsilon paths and
+// derivations of earlier rounds only), so expanding one terminates; the
+// strings are the expansions.  Item prefixes of a run's own entries follow a
+// breadth-first search over (class, item) from the start items at class j.
+void build_witness_strings(HostTables& H, int K, const std::vector<char>& epsp, int T, int N, int P,
+                           const int32_t* lhs, const int32_t* roff, const int32_t* rhs, const std::vector<int>& base) {
+  const int NI = H.NI, KK = std::max(K, 1), W = H.W;
+  constexpr size_t kPoolCap = (size_t)8 << 20;
+  H.wy_nt.assign((size_t)KK * KK * N, -1);
+  H.wy_own.assign((size_t)KK * KK * NI, -1);
+  H.wy_pool.clear();
+  if (K == 0) return;
+  struct Deriv {
+    int round = 0, prod = -1;
+    std::vector<int> cls;   // class after each symbol (cls[0]: after the leading epsilon path)
+    std::vector<int> via;   // terminal symbol i: the class its edge leaves from
+  };
+  std::vector<Deriv> der((size_t)K * K * N);
+  auto at = [&](int A, int j, int k) -> Deriv& { return der[((size_t)j * K + k) * N + A]; };
+  for (int round = 1;; ++round) {
+    std::vector<std::pair<size_t, Deriv>> found;
+    for (int p = 0; p < P; ++p) {
+      const int A = lhs[p] - T, m = roff[p + 1] - roff[p];
+      for (int j = 0; j < K; ++j) {
+        // pred[i][c]: class before symbol i reaching class c after it (-1: unreached);
+        // from[i][c]: for terminal symbols, the class the edge leaves from
+        std::vector<std::vector<int>> pred(m + 1, std::vector<int>(K, -1)), from(m + 1, std::vector<int>(K, -1));
+        for (int c = 0; c < K; ++c)
+          if (epsp[(size_t)j * K + c]) pred[0][c] = j;
+        for (int i = 1; i <= m; ++i) {
+          const int X = rhs[roff[p] + i - 1];
+          for (int c = 0; c < K; ++c) {
+            if (pred[i - 1][c] < 0) continue;
+            for (int c2 = 0; c2 < K; ++c2) {
+              if (X < T) {
+                if (!((H.cls_internal[(size_t)c * K + c2] >> X) & 1)) continue;
+                for (int c3 = 0; c3 < K; ++c3)
+                  if (epsp[(size_t)c2 * K + c3] && pred[i][c3] < 0) {
+                    pred[i][c3] = c;
+                    from[i][c3] = c2;
+                  }
+              } else {
+                const Deriv& d = at(X - T, c, c2);
+                if (d.prod >= 0 && d.round < round && pred[i][c2] < 0) pred[i][c2] = c;
+              }
+            }
+          }
+        }
+        for (int k = 0; k < K; ++k) {
+          if (pred[m][k] < 0 || at(A, j, k).prod >= 0) continue;
+          Deriv d;
+          d.round = round;
+          d.prod = p;
+          d.cls.assign(m + 1, 0);
+          d.via.assign(m + 1, -1);
+          int c = k;
+          for (int i = m; i >= 1; --i) {
+            d.cls[i] = c;
+            d.via[i] = from[i][c];
+            c = pred[i][c];
+          }
+          d.cls[0] = c;
+          found.push_back({((size_t)j * K + k) * N + A, d});
+        }
+      }
+    }
+    int added = 0;
+    for (auto& f : found)
+      if (der[f.first].prod < 0) {
+        der[f.first] = f.second;
+        ++added;
+      }
+    if (!added) break;
+  }
+  // expansions, memoised per (A, j, k)
+  std::vector<std::vector<uint8_t>> str((size_t)K * K * N);
+  std::vector<char> done((size_t)K * K * N, 0);
+  bool overflow = false;
+  std::function<const std::vector<uint8_t>&(int, int, int)> expand = [&](int A, int j, int k) -> const std::vector<uint8_t>& {
+    const size_t id = ((size_t)j * K + k) * N + A;
+    if (done[id]) return str[id];
+    const Deriv& d = der[id];
+    std::vector<uint8_t> out;
+    const int m = roff[d.prod + 1] - roff[d.prod];
+    for (int i = 1; i <= m && !overflow; ++i) {
+      const int X = rhs[roff[d.prod] + i - 1];
+      if (X < T) {
+        out.push_back((uint8_t)X);
+      } else {
+        const std::vector<uint8_t>& sub = expand(X - T, d.cls[i - 1], d.cls[i]);
+        out.insert(out.end(), sub.begin(), sub.end());
+      }
+      if (out.size() > 4096) overflow = true;
+    }
+    done[id] = 1;
+    str[id] = std::move(out);
+    return str[id];
+  };
+  auto put = [&](const std::vector<uint8_t>& v) -> int32_t {
+    if (v.size() > 0xFFFF || H.wy_pool.size() + v.size() + 2 > kPoolCap) return -1;
+    const int32_t off = (int32_t)H.wy_pool.size();
+    H.wy_pool.push_back((uint8_t)(v.size() & 0xFF));
+    H.wy_pool.push_back((uint8_t)(v.size() >> 8));
+    H.wy_pool.insert(H.wy_pool.end(), v.begin(), v.end());
+    return off;
+  };
+  for (int j = 0; j < K; ++j)
+    for (int k = 0; k < K; ++k)
+      for (int A = 0; A < N; ++A)
+        if (at(A, j, k).prod >= 0) {
+          overflow = false;
+          const std::vector<uint8_t>& v = expand(A, j, k);
+          if (!overflow) H.wy_nt[((size_t)j * K + k) * N + A] = put(v);
+        }
+  // item prefixes of a run's own entries: breadth-first over (class, item)
+  std::vector<int> prod_of(NI, -1);
+  for (int p = 0; p <= P; ++p) {
+    const int len = p < P ? roff[p + 1] - roff[p] : 1;
+    for (int d = 0; d <= len; ++d) prod_of[base[p] + d] = p;
+  }
+  for (int j = 0; j < K; ++j) {
+    std::vector<int> par((size_t)K * NI, -2);  // parent state, -1 for a start item at class j
+    std::vector<std::vector<uint8_t>> pre((size_t)K * NI);
+    std::vector<int> queue;
+    for (int p = 0; p < P; ++p) {
+      const int s = j * NI + base[p];
+      par[s] = -1;
+      queue.push_back(s);
+    }
+    for (size_t qi = 0; qi < queue.size(); ++qi) {
+      const int s = queue[qi], c = s / NI, it = s % NI;
+      auto visit = [&](int c2, int it2, const std::vector<uint8_t>* add) {
+        const int s2 = c2 * NI + it2;
+        if (par[s2] != -2) return;
+        par[s2] = s;
+        pre[s2] = pre[s];
+        if (add) pre[s2].insert(pre[s2].end(), add->begin(), add->end());
+        queue.push_back(s2);
+      };
+      for (int c2 = 0; c2 < K; ++c2)
+        if (c2 != c && epsp[(size_t)c * K + c2]) visit(c2, it, nullptr);
+      const int sym = H.next_sym[it];
+      if (sym < 0 || prod_of[it] >= P) continue;
+      for (int c2 = 0; c2 < K; ++c2) {
+        if (sym < 64) {
+          if ((H.cls_internal[(size_t)c * K + c2] >> sym) & 1) {
+            const std::vector<uint8_t> t{(uint8_t)sym};
+            visit(c2, it + 1, &t);
+          }
+        } else {
+          const int32_t off = H.wy_nt[((size_t)c * K + c2) * N + (sym - 64)];
+          if (off >= 0) {
+            const int len = H.wy_pool[off] | (H.wy_pool[off + 1] << 8);
+            const std::vector<uint8_t> t(H.wy_pool.begin() + off + 2, H.wy_pool.begin() + off + 2 + len);
+            visit(c2, it + 1, &t);
+          }
+        }
+      }
+    }
+    for (int k = 0; k < K; ++k)
+      for (int it = 0; it < NI; ++it)
+        if (par[(size_t)k * NI + it] != -2 && ((H.gap_own[((size_t)j * K + k) * W + (it >> 5)] >> (it & 31)) & 1))
+          H.wy_own[((size_t)j * K + k) * NI + it] = put(pre[(size_t)k * NI + it]);
+  }
+}
 
 }  // namespace
 
@@ -619,6 +788,10 @@ int build_tables(int Q, const int16_t* trans, const int16_t* accept, int T, int 
     for (int k = 0; k < K; ++k)
       for (int w = 0; w < W; ++w) H.gap_own[((size_t)j * K + k) * W + w] = x[k][w];
   }
+  // ---------------------------------------------------------------- witness strings
+  H.dot0.assign(W, 0);
+  for (int p = 0; p <= P; ++p) set32(H.dot0, 0, base[p]);
+  build_witness_strings(H, K, epsp, T, N, P, lhs, roff, rhs, base);
   return 0;
 }
 

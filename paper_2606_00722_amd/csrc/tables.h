@@ -65,6 +65,17 @@ struct HostTables {
   // is the set of states at class node k reachable from state s at class node j
   // (epsilon moves of the cover and the run's own labelled edges)
   std::vector<uint32_t> gap_cover;
+  // witness extraction (failure recovery): terminal strings of what a masked
+  // run derives between its class nodes.  A string in wy_pool is a 16-bit
+  // length followed by that many terminal ids; offsets are -1 where there is
+  // none.  wy_nt[(j*K + k)*N + B]: a string of L(B) labelling a path from class
+  // j to class k; wy_own[(j*K + k)*NI + i]: the symbols before the dot of item
+  // i (an item of the entry of the run's origin j at class k) derived along a
+  // path from class j to class k.
+  std::vector<int32_t> wy_nt;
+  std::vector<int32_t> wy_own;
+  std::vector<uint8_t> wy_pool;
+  std::vector<uint32_t> dot0;  // [W] items with the dot at the start of their production
   // vocabulary
   std::vector<uint8_t> vbytes;
   std::vector<int32_t> voffs;

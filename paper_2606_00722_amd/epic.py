@@ -27,6 +27,7 @@ FUNCTIONS = ["epic_ctx_create", "epic_ctx_destroy", "epic_workspace_bytes", "epi
              "epic_select_compatible",
              "epic_commit_fallback",
              "epic_ctx_device_error", "epic_ctx_work_counters", "epic_ctx_set_timing", "epic_ctx_kernel_stats",
+             "epic_witness_workspace_bytes", "epic_witness",
              "epic_diag_lds_stream", "epic_diag_clock_rates", "epic_status_string"]
 KERNEL_KINDS = ["lexmemo", "base", "validate", "select", "fallback", "spec_clear"]
 
@@ -91,6 +92,10 @@ def lib() -> ctypes.CDLL:
         L.epic_ctx_set_timing.restype = ctypes.c_int
         L.epic_ctx_kernel_stats.argtypes = [P, P, P, P, P]
         L.epic_ctx_kernel_stats.restype = ctypes.c_int
+        L.epic_witness_workspace_bytes.argtypes = [P, i32]
+        L.epic_witness_workspace_bytes.restype = sz
+        L.epic_witness.argtypes = [P, P, i32, i32, P, i32, P, i32, P, P, sz, P, sz, P]
+        L.epic_witness.restype = ctypes.c_int
         L.epic_diag_lds_stream.argtypes = [i32, i32, i32, P, P]
         L.epic_diag_lds_stream.restype = ctypes.c_int
         L.epic_diag_clock_rates.argtypes = [ctypes.POINTER(i32), ctypes.POINTER(i32)]
@@ -170,6 +175,12 @@ class Context:
 
         return torch.zeros(self.workspace_bytes + 256, dtype=torch.uint8, device=device)
 
+    def alloc_witness_workspace(self, B: int, device="cuda"):
+        """Device memory for epic_witness on B sequences (contents need not be cleared)."""
+        import torch
+
+        return torch.empty(self.witness_workspace_bytes(B) + 256, dtype=torch.uint8, device=device)
+
     def lexmemo_build(self, stream=None):
         _check("epic_lexmemo_build", lib().epic_lexmemo_build(self._h, _stream(stream)))
 
@@ -214,6 +225,20 @@ class Context:
         _check("epic_commit_fallback", lib().epic_commit_fallback(
             self._h, _ptr(seqs), B, n, _ptr(cand_seq), _ptr(cand_pos), _ptr(cand_tok), _ptr(conf), _ptr(verdict),
             _ptr(selected), _ptr(num_commit), int(cand_seq.numel()), _ptr(accepted), wp, wb, _stream(stream)))
+
+    def witness_workspace_bytes(self, B: int) -> int:
+        return int(lib().epic_witness_workspace_bytes(self._h, int(B)))
+
+    def witness(self, seqs, out_bytes, gap_len, status, witness_ws, workspace, stream=None):
+        """epic_witness: out_bytes uint8 [B, bytes_per_seq], gap_len int32
+        [B, max_gaps], status int32 [B]; witness_ws a uint8 tensor of
+        witness_workspace_bytes(B) bytes."""
+        B, n = int(seqs.shape[0]), int(seqs.shape[1])
+        wp, wb = self._ws(workspace)
+        wwp, wwb = self._ws(witness_ws)
+        _check("epic_witness", lib().epic_witness(
+            self._h, _ptr(seqs), B, n, _ptr(out_bytes), int(out_bytes.shape[1]), _ptr(gap_len), int(gap_len.shape[1]),
+            _ptr(status), wwp, wwb, wp, wb, _stream(stream)))
 
     def work_counters(self, stream=None) -> np.ndarray:
         """int64[6]: walks, chart entries written, memo entries read, graph nodes,

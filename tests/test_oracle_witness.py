@@ -109,3 +109,25 @@ def test_workload_sequences(oracle_lib):
                     y[rng.choice(fixed)] = rng.integers(0, inst.vocab.size)
                 seen.add(check_witness(oracle_lib, p, inst.lang, inst.vocab.strings, y))
         assert 1 in seen
+
+
+@pytest.mark.parametrize("preset,n", [(1, 24), (2, 32), (3, 24)])
+def test_valid_text_is_lexing_then_cyk(oracle_lib, preset, n):
+    """Valid of a plain byte string (what a completed output is checked with):
+    equal to regex maximal munch followed by CYK-style recognition, on the
+    hidden sentences of a workload and on corrupted copies of them."""
+    inst = W.make_instance(preset, 11, B=3, n=n)
+    p = oracle_lib.problem_from(inst.lang, inst.vocab)
+    rng = np.random.default_rng(preset)
+    seen = set()
+    for b in range(inst.B):
+        text = b"".join(inst.vocab.strings[t] for t in inst.hidden[b])
+        for k in range(4):
+            t2 = bytearray(text)
+            if k:
+                t2[int(rng.integers(0, len(t2)))] = int(rng.choice(list(set(text))))
+            toks = refimpl.munch_lex(inst.lang.name, t2.decode("latin-1"))
+            want = int(toks is not None and refimpl.derives(inst.lang.grammar, toks))
+            seen.add(want)
+            assert oracle_lib.valid_text(p, bytes(t2)) == want
+    assert seen == {0, 1}
