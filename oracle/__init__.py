@@ -65,6 +65,8 @@ def lib() -> ctypes.CDLL:
         L.oracle_select.argtypes = [P, P, P, P, i32, i32, P, P, P, P, P, i32, P, P, i32]
         L.oracle_witness.argtypes = [P, P, P, P, i32, P, i32, P, i32, P]
         L.oracle_valid_text.argtypes = [P, P, P, i32]
+        L.oracle_con_validate_batch.argtypes = [P, P, P, P, i32, i32, P, P, P, i32, P, P, i32]
+        L.oracle_con_dfa_states.argtypes = [P, P, P, P, i32]
         _lib = L
     return _lib
 
@@ -191,6 +193,29 @@ def witness(p: Problem, x):
         gaps.append(bytes(out[k:k + lens[j]]))
         k += int(lens[j])
     return 1, gaps
+
+
+def con_validate_batch(p: Problem, seqs: np.ndarray, seq, pos, tok, nthreads: int = 1):
+    """The prior pipeline ("Con.": lexing automaton, subset construction,
+    Hopcroft minimisation, intersection emptiness) on every candidate: returns
+    (verdict uint8[C], summed ms per phase [lex, dfa, val])."""
+    s = np.ascontiguousarray(seqs, dtype=np.int32)
+    cs, cp, ct = _cands(seq, pos, tok)
+    C = int(cs.size)
+    out = np.zeros(max(C, 1), dtype=np.uint8)
+    ms = np.zeros(3, dtype=np.float64)
+    lx, gr, vc = p.refs
+    r = lib().oracle_con_validate_batch(lx, gr, vc, _ptr(s), s.shape[0], s.shape[1], _ptr(cs) if C else 0,
+                                        _ptr(cp) if C else 0, _ptr(ct) if C else 0, C, _ptr(out), _ptr(ms), nthreads)
+    if r != 0:
+        raise RuntimeError(f"oracle_con_validate_batch failed ({r})")
+    return out[:C], ms
+
+
+def con_dfa_states(p: Problem, x) -> int:
+    xs = _seq(x)
+    lx, gr, vc = p.refs
+    return lib().oracle_con_dfa_states(lx, gr, vc, _ptr(xs) if xs.size else _ptr(np.zeros(1, np.int32)), int(xs.size))
 
 
 def valid_text(p: Problem, text: bytes) -> int:

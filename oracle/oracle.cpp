@@ -37,11 +37,17 @@
 //    terminates, give a terminal string of L(G) accepted by A_x; a breadth-first
 //    search of A_x finds a path spelling it; its moves inside masked runs give
 //    the bytes of each run.
+//  * The prior pipeline ("Con.", Sec. 2, App. A.1-A.2), a CPU comparator: the
+//    same automaton, determinised, minimised by Hopcroft's algorithm, then the
+//    emptiness of its intersection with the grammar (Bar-Hillel facts over a
+//    binarised grammar, by an agenda); timed per phase.
 //  * Select: Alg. 4 (RelaxedSelect then ExactShrink) over the candidates of a
 //    sequence whose individual verdict is 1, sorted by descending float32
 //    confidence with ties to the lower candidate index, halves split with the
 //    first ceil(|C|/2) candidates on the high-confidence side.
 #include <algorithm>
+#include <array>
+#include <chrono>
 #include <cstdio>
 #include <cstdlib>
 #include <atomic>
@@ -492,6 +498,199 @@ bool cover_accepts(const Cover& F, const DFA& D) {
   return false;
 }
 
+// ----- the prior pipeline ("Con."), a CPU comparator ---------------------------------
+// The earlier CFG-constrained decoder (Sec. 2; App. A.1-A.2) re-checks every
+// update from scratch: the lexing automaton of the partial output (an
+// epsilon-NFA over terminals, built here as for A_x), its determinisation
+// (subset construction) and minimisation (Hopcroft's partition refinement,
+// O(|Sigma| |Q| log |Q|)), then the emptiness of the intersection of the DFA
+// with the grammar (Bar-Hillel: facts (A, p, q), cubic in the DFA states).
+// The three phases are timed separately (the Lex / DFA / Val columns of
+// Tab. 2).  The verdict is the same criterion as Valid.
+
+// Hopcroft minimisation of D (missing transitions go to an implicit dead state)
+void hopcroft_minimize(DFA& D) {
+  const int n = D.states(), T = D.T, dead = n, m = n + 1;
+  if (n == 0) return;
+  auto tr = [&](int s, int a) { return s == dead ? dead : (D.trans[s][a] < 0 ? dead : D.trans[s][a]); };
+  // predecessors per (state, terminal)
+  std::vector<std::vector<std::vector<int>>> pre(T, std::vector<std::vector<int>>(m));
+  for (int st = 0; st < m; ++st)
+    for (int a = 0; a < T; ++a) pre[a][tr(st, a)].push_back(st);
+  std::vector<int> block(m);
+  std::vector<std::vector<int>> blocks;
+  std::vector<int> acc, rej;
+  for (int st = 0; st < m; ++st) (st < n && D.fin[st] ? acc : rej).push_back(st);
+  for (auto* part : {&acc, &rej})
+    if (!part->empty()) {
+      for (int st : *part) block[st] = (int)blocks.size();
+      blocks.push_back(*part);
+    }
+  std::deque<std::pair<int, int>> work;  // (block, terminal) splitters
+  std::set<std::pair<int, int>> in_work;
+  const int first = blocks.size() == 2 && blocks[0].size() > blocks[1].size() ? 1 : 0;
+  for (int a = 0; a < T; ++a) {
+    work.push_back({first, a});
+    in_work.insert({first, a});
+  }
+  while (!work.empty()) {
+    const auto [sb, a] = work.front();
+    work.pop_front();
+    in_work.erase({sb, a});
+    // X = states with an a-move into block sb
+    std::map<int, std::vector<int>> hit;  // block -> its states in X
+    for (int st : blocks[sb])
+      for (int pst : pre[a][st]) hit[block[pst]].push_back(pst);
+    for (auto& kv : hit) {
+      const int y = kv.first;
+      std::vector<int>& inx = kv.second;
+      std::sort(inx.begin(), inx.end());
+      inx.erase(std::unique(inx.begin(), inx.end()), inx.end());
+      if (inx.size() == blocks[y].size()) continue;  // no split
+      std::set<int> xs(inx.begin(), inx.end());
+      std::vector<int> rest;
+      for (int st : blocks[y])
+        if (!xs.count(st)) rest.push_back(st);
+      const int z = (int)blocks.size();
+      blocks[y] = inx;
+      blocks.push_back(rest);
+      for (int st : rest) block[st] = z;
+      for (int b = 0; b < T; ++b) {
+        if (in_work.count({y, b})) {
+          work.push_back({z, b});
+          in_work.insert({z, b});
+        } else {
+          const int small = blocks[y].size() <= blocks[z].size() ? y : z;
+          work.push_back({small, b});
+          in_work.insert({small, b});
+        }
+      }
+    }
+  }
+  // the minimal DFA: blocks reachable from the start, without the dead block
+  const int dead_block = block[dead];
+  std::vector<int> id(blocks.size(), -1);
+  std::vector<int> order{block[D.start]};
+  id[block[D.start]] = 0;
+  DFA M;
+  M.T = T;
+  for (size_t k = 0; k < order.size(); ++k) {
+    const int bl = order[k], rep = blocks[bl][0];
+    std::vector<int> row(T, -1);
+    for (int a = 0; a < T; ++a) {
+      const int to = block[tr(rep, a)];
+      if (to == dead_block) continue;
+      if (id[to] < 0) {
+        id[to] = (int)order.size();
+        order.push_back(to);
+      }
+      row[a] = id[to];
+    }
+    M.trans.push_back(row);
+    M.fin.push_back(rep < n && D.fin[rep]);
+  }
+  M.start = block[D.start] == dead_block ? -1 : 0;
+  if (M.start < 0) M = DFA{T, -1, {}, {}};
+  D = M;
+}
+
+// Emptiness of the intersection of L(G) and L(D): facts (X, p, q), symbol X
+// deriving a string that takes D from p to q, over the grammar binarised
+// (A -> X1 X2 ... Xk as a left-nested chain of fresh symbols), by an agenda.
+bool intersection_nonempty(const GrammarView& g, const DFA& D) {
+  if (D.start < 0) return false;
+  const int n = D.states(), T = g.T;
+  int nsym = T + g.N;
+  std::vector<std::pair<int, int>> unit;              // (A, X): A -> X
+  std::vector<std::array<int, 3>> bin;                 // (A, X, Y): A -> X Y
+  std::vector<int> eps_nt;
+  for (int pr = 0; pr < g.P; ++pr) {
+    const int A = g.lhs[pr];
+    const auto& r = g.rhs[pr];
+    if (r.empty()) {
+      eps_nt.push_back(A);
+    } else if (r.size() == 1) {
+      unit.push_back({A, r[0]});
+    } else {
+      int left = r[0];
+      for (size_t k = 1; k < r.size(); ++k) {
+        const int to = k + 1 == r.size() ? A : nsym++;
+        bin.push_back({to, left, r[k]});
+        left = to;
+      }
+    }
+  }
+  std::vector<std::vector<int>> by_unit(nsym), by_left(nsym), by_right(nsym);
+  for (size_t k = 0; k < unit.size(); ++k) by_unit[unit[k].second].push_back((int)k);
+  for (size_t k = 0; k < bin.size(); ++k) {
+    by_left[bin[k][1]].push_back((int)k);
+    by_right[bin[k][2]].push_back((int)k);
+  }
+  std::unordered_set<uint64_t> seen;
+  std::vector<std::vector<std::vector<int>>> out(nsym), in(nsym);  // [X][p] -> q, [X][q] -> p
+  std::vector<std::array<int, 3>> agenda;
+  auto add = [&](int X, int p, int q) {
+    const uint64_t key = ((uint64_t)X * n + p) * n + q;
+    if (!seen.insert(key).second) return;
+    if (out[X].empty()) {
+      out[X].assign(n, {});
+      in[X].assign(n, {});
+    }
+    out[X][p].push_back(q);
+    in[X][q].push_back(p);
+    agenda.push_back({X, p, q});
+  };
+  for (int p = 0; p < n; ++p) {
+    for (int a = 0; a < T; ++a)
+      if (D.trans[p][a] >= 0) add(a, p, D.trans[p][a]);
+    for (int A : eps_nt) add(A, p, p);
+  }
+  const int S = g.rhs[g.P][0];
+  while (!agenda.empty()) {
+    const auto f = agenda.back();
+    agenda.pop_back();
+    const int X = f[0], p = f[1], q = f[2];
+    if (X == S && p == D.start && D.fin[q]) return true;
+    for (int k : by_unit[X]) add(unit[k].first, p, q);
+    for (int k : by_left[X]) {  // A -> X Y
+      const int Y = bin[k][2];
+      if (!out[Y].empty())
+        for (size_t t = 0; t < out[Y][q].size(); ++t) add(bin[k][0], p, out[Y][q][t]);
+    }
+    for (int k : by_right[X]) {  // A -> Y X
+      const int Y = bin[k][1];
+      if (!in[Y].empty())
+        for (size_t t = 0; t < in[Y][p].size(); ++t) add(bin[k][0], in[Y][p][t], q);
+    }
+  }
+  return false;
+}
+
+// The prior pipeline on x: 1 / 0, or -3 on the DFA limit; ms[0..2] += the
+// lexing-automaton, determinise-and-minimise and intersection times.
+int con_check(const Lexer& L, const Grammar& G, const Vocab& V, const std::vector<int32_t>& x, double* ms,
+              int* dfa_states = nullptr) {
+  using clk = std::chrono::steady_clock;
+  const auto t0 = clk::now();
+  CharNFA A;
+  build_char_nfa(L, make_slots(V, x.data(), (int)x.size()), A);
+  const auto t1 = clk::now();
+  DFA D;
+  if (!determinize(A, G.T, D, 4000000)) return -3;
+  if (D.start >= 0) hopcroft_minimize(D);
+  const auto t2 = clk::now();
+  if (dfa_states) *dfa_states = D.start < 0 ? 0 : D.states();
+  GrammarView g(G);
+  const bool ok = intersection_nonempty(g, D);
+  const auto t3 = clk::now();
+  if (ms) {
+    ms[0] += std::chrono::duration<double, std::milli>(t1 - t0).count();
+    ms[1] += std::chrono::duration<double, std::milli>(t2 - t1).count();
+    ms[2] += std::chrono::duration<double, std::milli>(t3 - t2).count();
+  }
+  return ok ? 1 : 0;
+}
+
 // ----- per-sequence checks --------------------------------------------------------
 // 1 / 0, or -3 when the DFA construction exceeded its state limit
 int valid_seq(const Lexer& L, const Grammar& G, const Vocab& V, const std::vector<int32_t>& x) {
@@ -888,6 +1087,46 @@ int oracle_valid_text(const oracle_lexer* l, const oracle_grammar* g, const uint
   if (D.start >= 0) minimize(D);
   GrammarView gv(to_grammar(g));
   return earley_accepts(gv, D) ? 1 : 0;
+}
+
+// The prior pipeline ("Con.") on candidates, as oracle_validate_batch:
+// verdict[c] in {0, 1} (2 malformed); ms[0..2] = summed lexing-automaton,
+// determinise-and-minimise and intersection times over all candidates (the
+// threads' times added).  Returns 0, or -3 on the DFA limit.
+int oracle_con_validate_batch(const oracle_lexer* l, const oracle_grammar* g, const oracle_vocab* v,
+                              const int32_t* seqs, int B, int n, const int32_t* cseq, const int32_t* cpos,
+                              const int32_t* ctok, int C, uint8_t* verdict, double* ms, int nthreads) {
+  const Lexer L = to_lexer(l);
+  const Grammar G = to_grammar(g);
+  const Vocab V = to_vocab(v);
+  std::atomic<int> err{0};
+  std::vector<std::array<double, 3>> part(C, std::array<double, 3>{0, 0, 0});
+  run_parallel(C, nthreads, [&](int c) {
+    const int b = cseq[c], i = cpos[c], t = ctok[c];
+    if (b < 0 || b >= B || i < 0 || i >= n || t < 0 || t >= V.V || seqs[(size_t)b * n + i] >= 0) {
+      verdict[c] = 2;
+      return;
+    }
+    std::vector<int32_t> x(seqs + (size_t)b * n, seqs + (size_t)(b + 1) * n);
+    x[i] = t;
+    const int r = con_check(L, G, V, x, part[c].data());
+    if (r < 0) err = r;
+    verdict[c] = (uint8_t)(r < 0 ? 2 : r);
+  });
+  for (int k = 0; k < 3; ++k) ms[k] = 0;
+  for (auto& pc : part)
+    for (int k = 0; k < 3; ++k) ms[k] += pc[k];
+  return err.load();
+}
+
+// Number of states of x's completion DFA after Hopcroft minimisation (the
+// prior pipeline's), -3 on blow-up.
+int oracle_con_dfa_states(const oracle_lexer* l, const oracle_grammar* g, const oracle_vocab* v, const int32_t* x,
+                          int n) {
+  std::vector<int32_t> xs(x, x + n);
+  int st = 0;
+  const int r = con_check(to_lexer(l), to_grammar(g), to_vocab(v), xs, nullptr, &st);
+  return r < 0 ? r : st;
 }
 
 // Number of states of the minimal completion DFA of x (diagnostics), -3 on blow-up.
