@@ -468,6 +468,28 @@ def main() -> int:
         print("device error flags set by the fallback", file=sys.stderr)
         return 1
 
+    # witness extraction (failure recovery) for every sequence of the first
+    # steps, timed on its own: one call per step over the whole batch
+    wws = ctx.alloc_witness_workspace(inst.B, dev)
+    wbytes = torch.zeros((inst.B, 1 << 14), dtype=torch.uint8, device=dev)
+    wlen = torch.zeros((inst.B, inst.n), dtype=torch.int32, device=dev)
+    wst = torch.zeros(inst.B, dtype=torch.int32, device=dev)
+    ctx.witness(traj[0]["seqs"], wbytes, wlen, wst, wws, ws)  # warm
+    torch.cuda.synchronize()
+    wit_ms, wit_ok = [], 0
+    for d in traj[:4]:
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        ctx.witness(d["seqs"], wbytes, wlen, wst, wws, ws)
+        e1.record()
+        torch.cuda.synchronize()
+        wit_ms.append(e0.elapsed_time(e1))
+        wit_ok += int((wst == 1).sum().item())
+    del wws
+    if ctx.device_error() != 0:
+        print("device error flags set by the witness extraction", file=sys.stderr)
+        return 1
+
     ms = {"lexmemo": [], "validate": [], "select": []}
     for e in ev:
         ms["lexmemo"].append(e[0].elapsed_time(e[1]))
@@ -496,6 +518,12 @@ def main() -> int:
         kern[k] = {"ms_per_launch": st["ms"] / st["launches"], "launches_per_step": st["launches"] / args.steps,
                    "ms_per_step": st["ms"] / args.steps, "bytes": by, "launches": st["launches"],
                    "walks_per_step": int(st["work"][0]) / args.steps}
+    # the selection's helper workgroups (speculated checks) count apart
+    hw = kstats.get("select_helpers", {}).get("work")
+    spec = None
+    if hw is not None and "select" in kern:
+        spec = {"walks_per_step": round(int(hw[0]) / args.steps, 1),
+                "bytes_per_select_launch": round(walk_bytes(hw) / kern["select"]["launches"], 1)}
     dom = max(kern, key=lambda k: kern[k]["ms_per_step"])
     kd = kern[dom]
     ms_launch = kd["ms_per_launch"]
@@ -511,7 +539,9 @@ def main() -> int:
     else:
         # walk kernels: the chart's item sets are combined in LDS; algorithmic
         # LDS bytes per applied (task, entry) pair: advance mask, slot words
-        # read and ORed (3 x 4W), per chart entry written: its slot words (4W)
+        # read and ORed (3 x 4W), per chart entry written: its slot words (4W);
+        # for the selection, its own checks only (the helpers' speculated
+        # checks are reported apart)
         w = kstats[dom]["work"]
         lds_launch = float(w[5] * 12 * Wd + w[1] * 4 * Wd) / kd["launches"]
         lds_gbs = lds_launch / (ms_launch * 1e-3) / 1e9
@@ -549,8 +579,11 @@ def main() -> int:
         "kernels_ms": {k: {"ms_per_launch": round(v["ms_per_launch"], 4),
                            "launches_per_step": round(v["launches_per_step"], 3),
                            "walks_per_step": round(v["walks_per_step"], 1)} for k, v in kern.items()},
+        "select_speculation": spec,
         "fallback": {"ms_per_call": round(fallback_ms, 4), "commits_per_call": round(fb_commits / args.steps, 2),
                      "budget": "per sequence, all of its proposals", "in_step": False},
+        "witness": {"ms_per_call": round(float(np.mean(wit_ms)), 4), "sequences_per_call": inst.B,
+                    "completions": wit_ok, "calls": len(wit_ms)},
         "roofline": roof,
         "cpu_baseline": cpu,
     }

@@ -84,6 +84,7 @@ constexpr int kDoneChecks = 64;  // answered checks remembered per sequence by t
 #endif
 constexpr int kShareSelectLen = EPIC_SHARE_SELECT_LEN;
 constexpr int kMemoThreads = 256;
+constexpr int kSelectHelpOffset = 3 * 8;  // work-counter words from the selection's set to its helpers' set
 
 // ------------------------------------------------------------------ memo
 #ifndef EPIC_KERNEL_UNIT
@@ -581,6 +582,7 @@ __global__ void __launch_bounds__(NT) select_kernel(DevTab tb, const int32_t* __
   // running one speculated check hr of sequence b.  Both reach the walks
   // through the one call site of each check type below.
   const bool helper = (int)blockIdx.x >= B;
+  if (helper && threadIdx.x == 0) L.work_set = kSelectHelpOffset;  // speculated checks counted apart
   const int hi = helper ? (int)blockIdx.x - B : 0;
   const int nh = (int)gridDim.x / B - 1;  // helpers per sequence
   const int b = helper ? hi / nh : (int)blockIdx.x;
@@ -836,7 +838,11 @@ using namespace epic;
 
 // Kernel kinds for the diagnostics: each kind's walks add to a work-counter
 // set of its own, and with timing on each launch is bracketed by HIP events.
-enum : int { kKLexmemo = 0, kKBase, kKValidate, kKSelect, kKFallback, kKSpecClear, kKernelKinds };
+// kKSelectHelp: the work counters of the selection's helper workgroups (the
+// speculated checks), kept apart from the selection's own walks; it has no
+// launches of its own (its time is the selection's).
+enum : int { kKLexmemo = 0, kKBase, kKValidate, kKSelect, kKFallback, kKSpecClear, kKSelectHelp, kKernelKinds };
+static_assert((kKSelectHelp - kKSelect) * 8 == kSelectHelpOffset, "helper counter set");
 constexpr int kWorkCounters = 6;   // counters per set (see epic_ctx_work_counters)
 constexpr size_t kWorkOff = 64;    // byte offset of the counter sets in the error block
 constexpr size_t kErrBlock = 1024; // bytes of the error / counter block

@@ -29,7 +29,7 @@ FUNCTIONS = ["epic_ctx_create", "epic_ctx_destroy", "epic_workspace_bytes", "epi
              "epic_ctx_device_error", "epic_ctx_work_counters", "epic_ctx_set_timing", "epic_ctx_kernel_stats",
              "epic_witness_workspace_bytes", "epic_witness",
              "epic_diag_lds_stream", "epic_diag_clock_rates", "epic_status_string"]
-KERNEL_KINDS = ["lexmemo", "base", "validate", "select", "fallback", "spec_clear"]
+KERNEL_KINDS = ["lexmemo", "base", "validate", "select", "fallback", "spec_clear", "select_helpers"]
 
 
 class EpicError(RuntimeError):
@@ -253,9 +253,10 @@ class Context:
     def kernel_stats(self, stream=None) -> dict:
         """Per kernel kind (KERNEL_KINDS): summed event ms, launches and the
         int64[6] work counters of its walks (read and cleared)."""
-        ms = np.zeros(6, dtype=np.float64)
-        n = np.zeros(6, dtype=np.int64)
-        work = np.zeros(36, dtype=np.int64)
+        nk = len(KERNEL_KINDS)
+        ms = np.zeros(nk, dtype=np.float64)
+        n = np.zeros(nk, dtype=np.int64)
+        work = np.zeros(6 * nk, dtype=np.int64)
         _check("epic_ctx_kernel_stats", lib().epic_ctx_kernel_stats(self._h, _stream(stream), ms.ctypes.data,
                                                                     n.ctypes.data, work.ctypes.data))
         return {k: {"ms": float(ms[i]), "launches": int(n[i]), "work": work[6 * i:6 * i + 6].copy()}
