@@ -506,12 +506,13 @@ EPIC_INLINE int select_walk_body(const DevTab& tb, Lds<W>& L, const WgWork& wk, 
 }
 
 // A check walk kept as a function of its own for 16-word item sets in the
-// selection: at 1024 threads per workgroup (128 registers per lane) it
-// measured faster than the inlined walk, which spills in its inner loops
-// (C-like selection 29.9 against 31.7 ms per 256-token step, 4.27 against
-// 4.34 ms per 1024-token step), although the call frame costs more per-lane
-// scratch.  Narrower item sets, and the sequential fallback (512 threads,
-// where the inlined walk needs no scratch), inline it.
+// selection.  It measured faster than the inlined walk although its call
+// frame costs more per-lane scratch: at 1024 threads per workgroup (128
+// registers per lane), where the inlined walk spills in its inner loops,
+// 29.7 against 31.7 ms of C-like selection per 256-token step; at 512
+// threads, on checks resumed from base walks, 4.12 against 4.44 ms per
+// 1024-token step.  Narrower item sets, and the sequential fallback, inline
+// it.
 template <int W, bool COVER, bool SHARE>
 __device__ __attribute__((noinline)) int select_walk_call(const DevTab& tb, Lds<W>& L, const WgWork& wk,
                                                           const WsArgs& ws, const int32_t* __restrict__ seqs, int n,
@@ -1112,11 +1113,10 @@ template <int W>
 void launch_base(epic_ctx* c, const int32_t* seqs, int B, int n, int gb, const WsArgs& wa, hipStream_t stream) {
   KernelTimer kt(c, kKBase, stream);
   const DevTab tb = tab_for(c, kKBase);
-  if (W >= 16 && gb <= c->num_cus)
-    hipLaunchKernelGGL((base_kernel<W, kThreadsWide>), dim3(gb), dim3(kThreadsWide), 0, stream, tb, seqs, B, n, c->tag,
-                       wa);
-  else
-    hipLaunchKernelGGL((base_kernel<W, kThreads>), dim3(gb), dim3(kThreads), 0, stream, tb, seqs, B, n, c->tag, wa);
+  // 512 threads also for 16-word item sets: at 1024 (128 registers per
+  // lane) the walk spills and measured slower (C-like 1024-token base walks
+  // 1.13 against 1.10 ms)
+  hipLaunchKernelGGL((base_kernel<W, kThreads>), dim3(gb), dim3(kThreads), 0, stream, tb, seqs, B, n, c->tag, wa);
 }
 
 template <int W>
@@ -1165,7 +1165,10 @@ epic_status SelectLaunch<W>::run(epic_ctx* c, const int32_t* seqs, int B, int n,
     KernelTimer kt(c, kKSpecClear, stream);
     hipLaunchKernelGGL(spec_clear_kernel<W>, dim3((B * kSpec + 255) / 256), dim3(256), 0, stream, spec, B * kSpec);
   }
-  const bool wide = W >= 16 && grid <= c->num_cus;
+  // 1024 threads for 16-word item sets when every workgroup has a CU, except
+  // for checks resumed from base walks (shorter walks, where 512 threads
+  // measured faster: 4.12 against 4.25 ms per C-like 1024-token step)
+  const bool wide = W >= 16 && grid <= c->num_cus && !share;
   const DevTab tb = tab_for(c, kKSelect);
   KernelTimer kt(c, kKSelect, stream);
   if (wide && share)
