@@ -67,7 +67,8 @@ def copy_calibration(mib: int) -> int:
 
 
 KERNEL_KIND = {"lexmemo_kernel": "lexmemo", "base_kernel": "base", "validate_kernel": "validate",
-               "select_kernel": "select", "fallback_kernel": "fallback", "spec_clear_kernel": "spec_clear"}
+               "select_kernel": "select", "fallback_kernel": "fallback", "spec_clear_kernel": "spec_bookkeeping",
+               "spec_account_kernel": "spec_bookkeeping"}
 LDS_COUNTERS = ("SQ_INSTS_LDS_LOAD_BANDWIDTH", "SQ_INSTS_LDS_STORE_BANDWIDTH", "SQ_INSTS_LDS_ATOMIC_BANDWIDTH")
 XCDS = 8  # GRBM_GUI_ACTIVE is summed over the eight accelerator dies
 CUS = 256
@@ -518,12 +519,14 @@ def main() -> int:
         kern[k] = {"ms_per_launch": st["ms"] / st["launches"], "launches_per_step": st["launches"] / args.steps,
                    "ms_per_step": st["ms"] / args.steps, "bytes": by, "launches": st["launches"],
                    "walks_per_step": int(st["work"][0]) / args.steps}
-    # the selection's helper workgroups (speculated checks) count apart
-    hw = kstats.get("select_helpers", {}).get("work")
+    # "select" counts the checks Alg. 4 asks for (walked by the selection's
+    # workgroup, or by a helper whose result it took); speculated checks whose
+    # results it did not take count apart
+    hw = kstats.get("spec_unused", {}).get("work")
     spec = None
     if hw is not None and "select" in kern:
-        spec = {"walks_per_step": round(int(hw[0]) / args.steps, 1),
-                "bytes_per_select_launch": round(walk_bytes(hw) / kern["select"]["launches"], 1)}
+        spec = {"unused_walks_per_step": round(int(hw[0]) / args.steps, 1),
+                "unused_bytes_per_select_launch": round(walk_bytes(hw) / kern["select"]["launches"], 1)}
     dom = max(kern, key=lambda k: kern[k]["ms_per_step"])
     kd = kern[dom]
     ms_launch = kd["ms_per_launch"]

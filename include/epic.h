@@ -246,9 +246,11 @@ epic_status epic_ctx_set_timing(epic_ctx* ctx, int32_t enable);
 
 /* Diagnostics: synchronise `stream`, then read and clear, per kernel kind k
  * (0 lexing memo, 1 base walks of prefix sharing, 2 candidate walks of
- * validation, 3 selection (its own checks), 4 sequential fallback,
- * 5 speculation-state clear, 6 the selection's helper workgroups (speculated
- * checks; no launches of their own, their time is the selection's)): ms[k]
+ * validation, 3 selection (the checks Alg. 4 asks for, whether walked by the
+ * selection's workgroup or taken from a helper's speculated walk),
+ * 4 sequential fallback, 5 speculation bookkeeping (state clear, work
+ * accounting), 6 speculated checks whose results the selection did not take
+ * (no launches of their own, their time is the selection's)): ms[k]
  * the summed event durations of its timed launches, launches[k] their
  * number, work[k*6 .. k*6+5] the work counters of its walks (as
  * epic_ctx_work_counters).  Host arrays of 7, 7 and 42 elements. */

@@ -84,7 +84,6 @@ constexpr int kDoneChecks = 64;  // answered checks remembered per sequence by t
 #endif
 constexpr int kShareSelectLen = EPIC_SHARE_SELECT_LEN;
 constexpr int kMemoThreads = 256;
-constexpr int kSelectHelpOffset = 3 * 8;  // work-counter words from the selection's set to its helpers' set
 
 // ------------------------------------------------------------------ memo
 #ifndef EPIC_KERNEL_UNIT
@@ -542,6 +541,11 @@ EPIC_INLINE int select_walk(const DevTab& tb, Lds<W>& L, const WgWork& wk, const
 // h + ceil((m-h)/2) (the half passed), 5 on ceil(h/2) (it failed).  A
 // launch runs as many of them per sequence as the CUs hold.
 constexpr int kSpec = 6;  // state slots per sequence: slot 0 unused, checks 1..5
+// Speculation block of a selection launch over B sequences (int32 words):
+// state [B*kSpec], result [B*kSpec], consulted flag [B*kSpec], then the work
+// counters of each speculated check's walk (uint64 [B*kSpec][6]).
+constexpr int spec_work_word(int B) { return (3 * B * kSpec + 1) & ~1; }
+constexpr int spec_words(int B) { return spec_work_word(B) + 2 * 6 * B * kSpec; }
 constexpr long long kSpecWaitCycles = 4ll << 30;  // give up waiting on a helper after this many clocks
 __device__ inline bool spec_exact(int r) { return r != 2; }
 __device__ inline uint64_t spec_mask(int r, int m) {
@@ -554,6 +558,20 @@ template <int W>
 __global__ void spec_clear_kernel(int32_t* __restrict__ state, int count) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i < count) state[i] = 0;
+}
+
+// After a selection launch: the work of each speculated check's walk goes to
+// the selection's counters (`used`: the selection took its result, so the
+// walk is one of the algorithm's own checks) or to the speculation's.
+template <int W>
+__global__ void spec_account_kernel(const int32_t* __restrict__ spec, int B, unsigned long long* used,
+                                    unsigned long long* unused) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= B * kSpec) return;
+  const unsigned long long* w = reinterpret_cast<const unsigned long long*>(spec + spec_work_word(B)) + (size_t)i * 6;
+  if (w[0] == 0) return;
+  unsigned long long* to = spec[2 * B * kSpec + i] ? used : unused;
+  for (int k = 0; k < 6; ++k) atomicAdd(&to[k], w[k]);
 }
 
 template <int W, int NT, bool SHARE>
@@ -577,17 +595,22 @@ __global__ void __launch_bounds__(NT) select_kernel(DevTab tb, const int32_t* __
   __shared__ int done_n, done_hit;
   const WgWork wk = slot_work(ws, blockIdx.x);
   stage_tables<W>(tb, L);
-  int32_t* spec_state = spec;           // [B * kSpec]
-  int32_t* spec_res = spec + B * kSpec;  // [B * kSpec]
+  int32_t* spec_state = spec;               // [B * kSpec]
+  int32_t* spec_res = spec + B * kSpec;      // [B * kSpec]
+  int32_t* spec_used = spec + 2 * B * kSpec;  // [B * kSpec]: the selection took the result
   // Workgroups b < B run Alg. 4 for sequence b; the others are helpers, each
   // running one speculated check hr of sequence b.  Both reach the walks
   // through the one call site of each check type below.
   const bool helper = (int)blockIdx.x >= B;
-  if (helper && threadIdx.x == 0) L.work_set = kSelectHelpOffset;  // speculated checks counted apart
   const int hi = helper ? (int)blockIdx.x - B : 0;
   const int nh = (int)gridDim.x / B - 1;  // helpers per sequence
   const int b = helper ? hi / nh : (int)blockIdx.x;
   const int hr = helper ? 1 + hi % nh : 0;
+  // a speculated check's walk counts its work in its own slot; after the
+  // launch it goes to the selection's counters when the selection took the
+  // result, else to the speculation's (spec_account_kernel)
+  if (helper && threadIdx.x == 0)
+    L.work_to = reinterpret_cast<unsigned long long*>(spec + spec_work_word(B)) + (size_t)(b * kSpec + hr) * 6;
   const bool helpers = nh > 0;
   const int bad = select_setup<W>(tb, L, seqs, n, cseq, cpos, ctok, conf, verdict, C, b, helper ? nullptr : selected);
   if (helper) {
@@ -721,6 +744,7 @@ __global__ void __launch_bounds__(NT) select_kernel(DevTab tb, const int32_t* __
           if (st != 1) break;
           __builtin_amdgcn_s_sleep(8);
         }
+        if (res >= 0) spec_used[b * kSpec + q] = 1;
         L.sel_res = res;
       }
       if (q > 0) {
@@ -839,11 +863,12 @@ using namespace epic;
 
 // Kernel kinds for the diagnostics: each kind's walks add to a work-counter
 // set of its own, and with timing on each launch is bracketed by HIP events.
-// kKSelectHelp: the work counters of the selection's helper workgroups (the
-// speculated checks), kept apart from the selection's own walks; it has no
-// launches of its own (its time is the selection's).
+// kKSelectHelp: the work counters of the speculated checks whose results the
+// selection did not take (walked by its helper workgroups besides the
+// algorithm's own checks); it has no launches of its own (its time is the
+// selection's).  kKSpecClear times the speculation bookkeeping: the state
+// clear before a selection launch and the work accounting after it.
 enum : int { kKLexmemo = 0, kKBase, kKValidate, kKSelect, kKFallback, kKSpecClear, kKSelectHelp, kKernelKinds };
-static_assert((kKSelectHelp - kKSelect) * 8 == kSelectHelpOffset, "helper counter set");
 constexpr int kWorkCounters = 6;   // counters per set (see epic_ctx_work_counters)
 constexpr size_t kWorkOff = 64;    // byte offset of the counter sets in the error block
 constexpr size_t kErrBlock = 1024; // bytes of the error / counter block
@@ -1163,26 +1188,37 @@ epic_status SelectLaunch<W>::run(epic_ctx* c, const int32_t* seqs, int B, int n,
   if (share) launch_base<W>(c, seqs, B, n, 2 * B, wa, stream);
   {
     KernelTimer kt(c, kKSpecClear, stream);
-    hipLaunchKernelGGL(spec_clear_kernel<W>, dim3((B * kSpec + 255) / 256), dim3(256), 0, stream, spec, B * kSpec);
+    hipLaunchKernelGGL(spec_clear_kernel<W>, dim3((spec_words(B) + 255) / 256), dim3(256), 0, stream, spec,
+                       spec_words(B));
   }
   // 1024 threads for 16-word item sets when every workgroup has a CU, except
   // for checks resumed from base walks (shorter walks, where 512 threads
   // measured faster: 4.12 against 4.25 ms per C-like 1024-token step)
   const bool wide = W >= 16 && grid <= c->num_cus && !share;
+  // The 1024-thread instance of the resumed-check selection is compiled but
+  // not launched: the out-of-line check walk that both instances call is then
+  // compiled to the 1024-thread register budget (128 per lane), and that code
+  // measured faster at 512 threads too (4.13 against 4.40 ms of C-like
+  // selection per 1024-token step) than a walk compiled for 512 threads only.
+  if constexpr (W >= 16) (void)&select_kernel<W, kThreadsWide, true>;
   const DevTab tb = tab_for(c, kKSelect);
-  KernelTimer kt(c, kKSelect, stream);
-  if (wide && share)
-    hipLaunchKernelGGL((select_kernel<W, kThreadsWide, true>), dim3(grid), dim3(kThreadsWide), 0, stream, tb, seqs, B,
-                       n, cs, cp, ct, conf, verdict, C, sel, (long long*)counts, spec, wa);
-  else if (wide)
-    hipLaunchKernelGGL((select_kernel<W, kThreadsWide, false>), dim3(grid), dim3(kThreadsWide), 0, stream, tb, seqs,
-                       B, n, cs, cp, ct, conf, verdict, C, sel, (long long*)counts, spec, wa);
-  else if (share)
-    hipLaunchKernelGGL((select_kernel<W, kThreads, true>), dim3(grid), dim3(kThreads), 0, stream, tb, seqs, B, n, cs,
-                       cp, ct, conf, verdict, C, sel, (long long*)counts, spec, wa);
-  else
-    hipLaunchKernelGGL((select_kernel<W, kThreads, false>), dim3(grid), dim3(kThreads), 0, stream, tb, seqs, B, n, cs,
-                       cp, ct, conf, verdict, C, sel, (long long*)counts, spec, wa);
+  {
+    KernelTimer kt(c, kKSelect, stream);
+    if (wide)
+      hipLaunchKernelGGL((select_kernel<W, kThreadsWide, false>), dim3(grid), dim3(kThreadsWide), 0, stream, tb, seqs,
+                         B, n, cs, cp, ct, conf, verdict, C, sel, (long long*)counts, spec, wa);
+    else if (share)
+      hipLaunchKernelGGL((select_kernel<W, kThreads, true>), dim3(grid), dim3(kThreads), 0, stream, tb, seqs, B, n,
+                         cs, cp, ct, conf, verdict, C, sel, (long long*)counts, spec, wa);
+    else
+      hipLaunchKernelGGL((select_kernel<W, kThreads, false>), dim3(grid), dim3(kThreads), 0, stream, tb, seqs, B, n,
+                         cs, cp, ct, conf, verdict, C, sel, (long long*)counts, spec, wa);
+  }
+  if (grid > B) {
+    KernelTimer kt(c, kKSpecClear, stream);
+    hipLaunchKernelGGL(spec_account_kernel<W>, dim3((B * kSpec + 255) / 256), dim3(256), 0, stream, spec, B,
+                       tb.work, tab_for(c, kKSelectHelp).work);
+  }
   return hipGetLastError() == hipSuccess ? EPIC_OK : EPIC_ERR_HIP;
 }
 
@@ -1455,7 +1491,7 @@ epic_status epic_ctx_create(const epic_lexer_desc* lexer, const epic_grammar_des
   c->off_snap = c->slot_bytes * (size_t)(c->nslot + 2 * c->base_slots);
   c->off_bseq = c->off_snap + c->snap_bytes * 2 * c->base_slots;
   c->off_spec = c->off_bseq + align256((size_t)2 * c->base_slots * max_seq_len * 4);
-  c->ws_bytes = c->off_spec + align256((size_t)c->max_batch * kSpec * 8);  // + speculated checks
+  c->ws_bytes = c->off_spec + align256((size_t)spec_words(c->max_batch) * 4);  // + speculated checks
   // witness workspace, per sequence: edge record, on-path marks (one bit per
   // chart item), search stack, witness terminals, byte-search records and
   // visited set, stored proofs and their index

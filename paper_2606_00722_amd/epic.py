@@ -29,7 +29,7 @@ FUNCTIONS = ["epic_ctx_create", "epic_ctx_destroy", "epic_workspace_bytes", "epi
              "epic_ctx_device_error", "epic_ctx_work_counters", "epic_ctx_set_timing", "epic_ctx_kernel_stats",
              "epic_witness_workspace_bytes", "epic_witness",
              "epic_diag_lds_stream", "epic_diag_clock_rates", "epic_status_string"]
-KERNEL_KINDS = ["lexmemo", "base", "validate", "select", "fallback", "spec_clear", "select_helpers"]
+KERNEL_KINDS = ["lexmemo", "base", "validate", "select", "fallback", "spec_bookkeeping", "spec_unused"]
 
 
 class EpicError(RuntimeError):
