@@ -333,6 +333,9 @@ def main() -> int:
     ap.add_argument("--preset", type=int, default=5,
                     help="workload preset 1..5 (default 5: C-like, 64 x 1024 tokens, the largest configuration)")
     ap.add_argument("--seed", type=int, default=42)
+    ap.add_argument("--saturate", type=int, default=1, metavar="K",
+                    help="saturated variant: the same configuration with K times the batch (same grammar and "
+                         "vocabulary; K = 16 gives every CU several walks); reports the step loop only")
     ap.add_argument("--cpu-seconds", type=float, default=24.0,
                     help="time budget of the oracle baseline (all legs together)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -366,7 +369,8 @@ def main() -> int:
     from paper_2606_00722_amd import workloads as W
 
     dev = torch.device("cuda:0")
-    inst = W.make_instance(args.preset, args.seed)
+    base_B = W.PRESETS[args.preset]["B"]
+    inst = W.make_instance(args.preset, args.seed, B=base_B * args.saturate if args.saturate > 1 else None)
     arr = W.arrays(inst.lang, inst.vocab)
     props_per_step = inst.cfg["props"] * inst.B
     ctx = epic.Context.from_problem(arr, inst.B, inst.n, props_per_step)
@@ -442,54 +446,56 @@ def main() -> int:
         print("device error flags set", file=sys.stderr)
         return 1
 
-    # the sequential fallback after the batch (Alg. 1), timed on its own over
-    # the same steps: per sequence a budget of all its proposals, so that the
-    # loop checks every valid candidate the batch left
-    fb_ms, fb_commits = [], 0
-    for d in traj:
-        nc = np.bincount(d["host"][1].seq, minlength=inst.B).astype(np.int32)
-        d["nc"] = t(nc)
-        d["accepted"] = torch.zeros(d["C"], dtype=torch.uint8, device=dev)
-    for d in traj[:2]:  # warm
-        ctx.fallback(d["seqs"], d["cs"], d["cp"], d["ct"], d["cf"], d["verdict"], d["selected"], d["nc"],
-                     d["accepted"], ws)
-    torch.cuda.synchronize()
-    for k in range(args.steps):
-        d = traj[k % len(traj)]
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        ctx.fallback(d["seqs"], d["cs"], d["cp"], d["ct"], d["cf"], d["verdict"], d["selected"], d["nc"],
-                     d["accepted"], ws)
-        e1.record()
-        fb_ms.append((e0, e1))
-    torch.cuda.synchronize()
-    for k in range(args.steps):
-        fb_commits += int(traj[k % len(traj)]["accepted"].sum().item())
-    if ctx.device_error() != 0:
-        print("device error flags set by the fallback", file=sys.stderr)
-        return 1
-
-    # witness extraction (failure recovery) for every sequence of the first
-    # steps, timed on its own: one call per step over the whole batch
-    wws = ctx.alloc_witness_workspace(inst.B, dev)
-    wbytes = torch.zeros((inst.B, 1 << 14), dtype=torch.uint8, device=dev)
-    wlen = torch.zeros((inst.B, inst.n), dtype=torch.int32, device=dev)
-    wst = torch.zeros(inst.B, dtype=torch.int32, device=dev)
-    ctx.witness(traj[0]["seqs"], wbytes, wlen, wst, wws, ws)  # warm
-    torch.cuda.synchronize()
-    wit_ms, wit_ok = [], 0
-    for d in traj[:4]:
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        ctx.witness(d["seqs"], wbytes, wlen, wst, wws, ws)
-        e1.record()
+    fb_ms, fb_commits, wit_ms, wit_ok = [], 0, [], 0
+    if args.saturate == 1:
+        # the sequential fallback after the batch (Alg. 1), timed on its own over
+        # the same steps: per sequence a budget of all its proposals, so that the
+        # loop checks every valid candidate the batch left
+        fb_ms, fb_commits = [], 0
+        for d in traj:
+            nc = np.bincount(d["host"][1].seq, minlength=inst.B).astype(np.int32)
+            d["nc"] = t(nc)
+            d["accepted"] = torch.zeros(d["C"], dtype=torch.uint8, device=dev)
+        for d in traj[:2]:  # warm
+            ctx.fallback(d["seqs"], d["cs"], d["cp"], d["ct"], d["cf"], d["verdict"], d["selected"], d["nc"],
+                         d["accepted"], ws)
         torch.cuda.synchronize()
-        wit_ms.append(e0.elapsed_time(e1))
-        wit_ok += int((wst == 1).sum().item())
-    del wws
-    if ctx.device_error() != 0:
-        print("device error flags set by the witness extraction", file=sys.stderr)
-        return 1
+        for k in range(args.steps):
+            d = traj[k % len(traj)]
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            ctx.fallback(d["seqs"], d["cs"], d["cp"], d["ct"], d["cf"], d["verdict"], d["selected"], d["nc"],
+                         d["accepted"], ws)
+            e1.record()
+            fb_ms.append((e0, e1))
+        torch.cuda.synchronize()
+        for k in range(args.steps):
+            fb_commits += int(traj[k % len(traj)]["accepted"].sum().item())
+        if ctx.device_error() != 0:
+            print("device error flags set by the fallback", file=sys.stderr)
+            return 1
+
+        # witness extraction (failure recovery) for every sequence of the first
+        # steps, timed on its own: one call per step over the whole batch
+        wws = ctx.alloc_witness_workspace(inst.B, dev)
+        wbytes = torch.zeros((inst.B, 1 << 14), dtype=torch.uint8, device=dev)
+        wlen = torch.zeros((inst.B, inst.n), dtype=torch.int32, device=dev)
+        wst = torch.zeros(inst.B, dtype=torch.int32, device=dev)
+        ctx.witness(traj[0]["seqs"], wbytes, wlen, wst, wws, ws)  # warm
+        torch.cuda.synchronize()
+        wit_ms, wit_ok = [], 0
+        for d in traj[:4]:
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            ctx.witness(d["seqs"], wbytes, wlen, wst, wws, ws)
+            e1.record()
+            torch.cuda.synchronize()
+            wit_ms.append(e0.elapsed_time(e1))
+            wit_ok += int((wst == 1).sum().item())
+        del wws
+        if ctx.device_error() != 0:
+            print("device error flags set by the witness extraction", file=sys.stderr)
+            return 1
 
     ms = {"lexmemo": [], "validate": [], "select": []}
     for e in ev:
@@ -497,7 +503,7 @@ def main() -> int:
         ms["validate"].append(e[1].elapsed_time(e[2]))
         ms["select"].append(e[2].elapsed_time(e[3]))
     phase = {k: float(np.mean(v)) for k, v in ms.items()}
-    fallback_ms = float(np.mean([a.elapsed_time(b) for a, b in fb_ms]))
+    fallback_ms = float(np.mean([a.elapsed_time(b) for a, b in fb_ms])) if fb_ms else None
 
     # algorithmic bytes of the walks of one kernel kind, from its work
     # counters over the timed steps: chart entries written (4W B of items,
@@ -532,7 +538,7 @@ def main() -> int:
     ms_launch = kd["ms_per_launch"]
     hbm_launch = kd["bytes"] / kd["launches"]
     hbm_gbs = hbm_launch / (ms_launch * 1e-3) / 1e9
-    pmc = pmc_summary(dom, args.preset)
+    pmc = pmc_summary(dom, args.preset) if args.saturate == 1 else None  # counters are of the default workload
     peak = lds_peak_record()
     lds_peak_gbs = peak["peak_gbs"] if peak else None
     if dom == "lexmemo":  # the one HBM-bound kernel: no LDS traffic
@@ -566,7 +572,7 @@ def main() -> int:
                             "lds_bank_conflict_per_active_cycle": pmc.get("lds_bank_conflict_per_active_cycle")}
 
     cpu = None
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and args.saturate == 1:
         log("cpu baseline")
         cpu = cpu_baseline(inst, traj, args.cpu_seconds)
 
@@ -575,18 +581,22 @@ def main() -> int:
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(1e3 * elapsed / args.steps, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "u32", "data": "synthetic",
         "source_hash": source_hash(),
-        "config": {"workload": W.PRESET_NAMES[args.preset], "preset": args.preset, "batch": inst.B,
-                   "seq_len": inst.n, "candidates_per_step": props_per_step, "steps_cycled": len(traj),
-                   "seed": args.seed, "parallelism": "none (1 GPU)"},
-        "phases_ms": {**{k: round(v, 4) for k, v in phase.items()}, "fallback": round(fallback_ms, 4)},
+        "config": {"workload": W.PRESET_NAMES[args.preset] + (
+                       f"; saturated: the batch x{args.saturate} ({inst.B} sequences, same grammar and vocabulary)"
+                       if args.saturate > 1 else ""),
+                   "preset": args.preset, "batch": inst.B, "seq_len": inst.n,
+                   "candidates_per_step": props_per_step, "steps_cycled": len(traj), "seed": args.seed,
+                   "saturated": args.saturate > 1, "parallelism": "none (1 GPU)"},
+        "phases_ms": {**{k: round(v, 4) for k, v in phase.items()},
+                      "fallback": round(fallback_ms, 4) if fallback_ms is not None else None},
         "kernels_ms": {k: {"ms_per_launch": round(v["ms_per_launch"], 4),
                            "launches_per_step": round(v["launches_per_step"], 3),
                            "walks_per_step": round(v["walks_per_step"], 1)} for k, v in kern.items()},
         "select_speculation": spec,
         "fallback": {"ms_per_call": round(fallback_ms, 4), "commits_per_call": round(fb_commits / args.steps, 2),
-                     "budget": "per sequence, all of its proposals", "in_step": False},
+                     "budget": "per sequence, all of its proposals", "in_step": False} if fb_ms else None,
         "witness": {"ms_per_call": round(float(np.mean(wit_ms)), 4), "sequences_per_call": inst.B,
-                    "completions": wit_ok, "calls": len(wit_ms)},
+                    "completions": wit_ok, "calls": len(wit_ms)} if wit_ms else None,
         "roofline": roof,
         "cpu_baseline": cpu,
     }

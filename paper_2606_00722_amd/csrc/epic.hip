@@ -1486,7 +1486,7 @@ epic_status epic_ctx_create(const epic_lexer_desc* lexer, const epic_grammar_des
   c->off_bits = c->off_st + align256((size_t)c->maxe * 8);
   c->off_cov = c->off_bits + align256((size_t)c->maxe * H.W * 4);
   c->slot_bytes = c->off_cov + align256((size_t)c->maxn * H.CW * 4);
-  c->base_slots = std::min(max_batch, 256);
+  c->base_slots = std::min(max_batch, 1024);
   c->snap_bytes = align256(kSnapHeader + (size_t)(max_seq_len / 2 + 1) * sizeof(Snapshot));
   c->off_snap = c->slot_bytes * (size_t)(c->nslot + 2 * c->base_slots);
   c->off_bseq = c->off_snap + c->snap_bytes * 2 * c->base_slots;

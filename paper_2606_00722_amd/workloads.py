@@ -60,7 +60,7 @@ PRESET_NAMES = {
     2: "json-like: vocab 4096, 8x128 tokens, mask U[0.25,0.75], 64 proposals/step, 8 steps",
     3: "smiles-like: vocab 8192, 16x256 tokens, 60% masked, 128 proposals/step, 16 steps",
     4: "c-like: vocab 32768, 16x256 tokens, 70% masked, 256 proposals/step, 4 steps",
-    5: "c-like: vocab 32768, 64x1024 tokens in 32-token blocks, 1024 proposals/step, 32 steps",
+    5: "c-like: vocab 32768, 64x1024 tokens in 32-token blocks, up to 16 proposals/seq (1024/step) in the active block, 32 steps",
 }
 
 
