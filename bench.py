@@ -68,7 +68,7 @@ def copy_calibration(mib: int) -> int:
 
 KERNEL_KIND = {"lexmemo_kernel": "lexmemo", "base_kernel": "base", "validate_kernel": "validate",
                "select_kernel": "select", "fallback_kernel": "fallback", "spec_clear_kernel": "spec_bookkeeping",
-               "spec_account_kernel": "spec_bookkeeping"}
+               "spec_account_kernel": "spec_bookkeeping", "base_validate_kernel": "validate"}
 LDS_COUNTERS = ("SQ_INSTS_LDS_LOAD_BANDWIDTH", "SQ_INSTS_LDS_STORE_BANDWIDTH", "SQ_INSTS_LDS_ATOMIC_BANDWIDTH")
 XCDS = 8  # GRBM_GUI_ACTIVE is summed over the eight accelerator dies
 CUS = 256

@@ -214,15 +214,17 @@ EPIC_INLINE void resume_from_base(Lds<W>& L, const WsArgs& a, int rec, int run, 
 // the first token that differs from the sequence the record was walked on
 // (the token there is then walked as the sequence now has it), and a record
 // of the very same sequence is kept as it is.
+// Base walk number blk (blk < B: the Earley graph of sequence blk; else the
+// cover graph of sequence blk - B).  With a nonzero epoch the record's
+// progress is published for walks of the same launch (publish_record).
 template <int W, int NT>
-__global__ void __launch_bounds__(NT) base_kernel(DevTab tb, const int32_t* __restrict__ seqs, int B, int n,
-                                                  uint64_t tag, WsArgs ws) {
-  __shared__ Lds<W> L;
-  const bool cov = (int)blockIdx.x >= B;
-  const int b = cov ? blockIdx.x - B : blockIdx.x;
+EPIC_INLINE void base_body(const DevTab& tb, Lds<W>& L, const int32_t* __restrict__ seqs, int B, int n, uint64_t tag,
+                           const WsArgs& ws, int blk, uint32_t epoch) {
+  const bool cov = blk >= B;
+  const int b = cov ? blk - B : blk;
   const int rec = cov ? ws.base_slots + b : b;
   WgWork wk = slot_work(ws, ws.nslot + rec);
-  stage_tables<W>(tb, L);
+  if (threadIdx.x == 0) L.epoch = epoch;
   char* snap = snap_record(ws, rec);
   int32_t* h = reinterpret_cast<int32_t*>(snap);
   int32_t* walked = reinterpret_cast<int32_t*>(ws.base + ws.bseq_off) + (size_t)rec * ws.max_seq;
@@ -248,7 +250,10 @@ __global__ void __launch_bounds__(NT) base_kernel(DevTab tb, const int32_t* __re
     return;
   }
   int d = L.minp < nold ? L.minp : nold;
-  if (owned && d == n && nold == n) return;  // the record is this sequence's
+  if (owned && d == n && nold == n) {  // the record is this sequence's
+    publish_record(L, snap, kRecDone | (uint32_t)h[1]);
+    return;
+  }
   const int runs = owned ? h[1] : 0;
   const Snapshot* sp0 = reinterpret_cast<const Snapshot*>(snap + kSnapHeader);
   for (int r = threadIdx.x; r < runs; r += NT)
@@ -266,23 +271,48 @@ __global__ void __launch_bounds__(NT) base_kernel(DevTab tb, const int32_t* __re
     h[4] = (int32_t)(uint32_t)tag;
     h[5] = (int32_t)(uint32_t)(tag >> 32);
   }
+  publish_record(L, snap, (uint32_t)(r0 >= 0 ? r0 : 0));  // snapshots before r0 stay as they are
   if (cov)
     walk<W, W, true>(tb, L, wk, n, i0, r0 >= 0, snap, r0 >= 0 ? r0 : 0);
   else
     walk<W, W, false>(tb, L, wk, n, i0, r0 >= 0, snap, r0 >= 0 ? r0 : 0);
 }
 
-// ------------------------------------------------------------------ validate
-template <int W, int NT, bool SHARE>
-__global__ void __launch_bounds__(NT) validate_kernel(DevTab tb, const int32_t* __restrict__ seqs, int B,
-                                                            int n, const int32_t* __restrict__ cseq,
-                                                            const int32_t* __restrict__ cpos,
-                                                            const int32_t* __restrict__ ctok, int C,
-                                                            uint8_t* __restrict__ verdict, WsArgs ws) {
+template <int W, int NT>
+__global__ void __launch_bounds__(NT) base_kernel(DevTab tb, const int32_t* __restrict__ seqs, int B, int n,
+                                                  uint64_t tag, WsArgs ws) {
   __shared__ Lds<W> L;
-  const WgWork wk = slot_work(ws, blockIdx.x);
   stage_tables<W>(tb, L);
-  for (int c = blockIdx.x; c < C; c += gridDim.x) {
+  base_body<W, NT>(tb, L, seqs, B, n, tag, ws, blockIdx.x, 0u);
+}
+
+// Thread 0: wait until walk record `snap` holds the snapshot of masked run
+// `run` written in launch `epoch`, or is final.  Returns the progress word,
+// or 0 when the wait timed out (the caller then walks from the start).
+constexpr long long kRecWaitCycles = 4ll << 30;
+__device__ inline uint64_t wait_record(const char* snap, uint32_t epoch, int run) {
+  const uint64_t* p = reinterpret_cast<const uint64_t*>(snap + 24);
+  const long long t_start = (long long)clock64();
+  for (;;) {
+    const uint64_t v = __hip_atomic_load(p, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
+    const uint32_t st = (uint32_t)v;
+    if ((uint32_t)(v >> 32) == epoch && ((st & kRecDone) || (int)st > run)) return v;
+    if ((long long)clock64() - t_start > kRecWaitCycles) return 0;
+    __builtin_amdgcn_s_sleep(8);
+  }
+}
+
+// ------------------------------------------------------------------ validate
+// Candidate walks blk, blk + nblk, ... in walk slot blk.  With SHARE each
+// resumes from its sequence's base walk; with a nonzero epoch those base
+// walks run in the same launch and the walk first waits for its snapshot.
+template <int W, int NT, bool SHARE>
+EPIC_INLINE void validate_body(const DevTab& tb, Lds<W>& L, const int32_t* __restrict__ seqs, int B, int n,
+                               const int32_t* __restrict__ cseq, const int32_t* __restrict__ cpos,
+                               const int32_t* __restrict__ ctok, int C, uint8_t* __restrict__ verdict,
+                               const WsArgs& ws, int blk, int nblk, uint32_t epoch) {
+  const WgWork wk = slot_work(ws, blk);
+  for (int c = blk; c < C; c += nblk) {
     const int b = cseq[c], i = cpos[c], t = ctok[c];
     const bool bad = b < 0 || b >= B || i < 0 || i >= n || t < 0 || t >= tb.V || seqs[(size_t)b * n + i] >= 0;
     if (bad) {
@@ -325,8 +355,21 @@ __global__ void __launch_bounds__(NT) validate_kernel(DevTab tb, const int32_t* 
       __syncthreads();
       const int run = L.rep_b;
       const int32_t* h = reinterpret_cast<const int32_t*>(snap_record(ws, b));
-      const int status = h[0], runs = h[1];
-      if (run < runs) {
+      int ready = 1;  // 1: the record is final; 2: snapshot `run` is written; 0: not waited for in time
+      if (epoch) {
+        __syncthreads();
+        if (threadIdx.x == 0) {
+          const uint64_t v = wait_record(snap_record(ws, b), epoch, run);
+          L.result = v == 0 ? 0 : (((uint32_t)v & kRecDone) ? 1 : 2);
+        }
+        __syncthreads();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+        ready = L.result;
+      }
+      const int status = ready == 1 ? h[0] : 0, runs = ready == 1 ? h[1] : run + 1;
+      if (ready == 0) {
+        r = walk<W, W, false>(tb, L, wk, n);
+      } else if (run < runs) {
         WgWork wr = wk;
         resume_from_base<W>(L, ws, b, run, wr);
         r = walk<W, W, false>(tb, L, wr, n, p0, true);
@@ -342,6 +385,43 @@ __global__ void __launch_bounds__(NT) validate_kernel(DevTab tb, const int32_t* 
       if (r < 0) atomicOr(tb.dev_err, (uint32_t)EPIC_DEV_CAPACITY | (1u << (8 + (L.overflow & 15))));
     }
     __syncthreads();
+  }
+}
+
+template <int W, int NT, bool SHARE>
+__global__ void __launch_bounds__(NT) validate_kernel(DevTab tb, const int32_t* __restrict__ seqs, int B,
+                                                            int n, const int32_t* __restrict__ cseq,
+                                                            const int32_t* __restrict__ cpos,
+                                                            const int32_t* __restrict__ ctok, int C,
+                                                            uint8_t* __restrict__ verdict, WsArgs ws) {
+  __shared__ Lds<W> L;
+  stage_tables<W>(tb, L);
+  validate_body<W, NT, SHARE>(tb, L, seqs, B, n, cseq, cpos, ctok, C, verdict, ws, blockIdx.x, gridDim.x, 0u);
+}
+
+// Base walks and the candidate walks that resume from them in one launch:
+// workgroups 0 .. gb-1 are the base walks (as base_kernel), the others the
+// candidate walks (as validate_kernel), each of which waits until the base
+// walk of its sequence has written the snapshot it resumes from, so that
+// candidate walks overlap the rest of the base walks.  Base walks have the
+// lowest workgroup numbers and wait on nothing, so they are dispatched first
+// and finish; a candidate walk that is not released in time walks from the
+// start instead.  The base walks' work counts apart (base_work).
+template <int W, int NT>
+__global__ void __launch_bounds__(NT) base_validate_kernel(DevTab tb, const int32_t* __restrict__ seqs, int B, int n,
+                                                           uint64_t tag, int gb, const int32_t* __restrict__ cseq,
+                                                           const int32_t* __restrict__ cpos,
+                                                           const int32_t* __restrict__ ctok, int C,
+                                                           uint8_t* __restrict__ verdict, WsArgs ws, uint32_t epoch,
+                                                           unsigned long long* base_work) {
+  __shared__ Lds<W> L;
+  stage_tables<W>(tb, L);
+  if ((int)blockIdx.x < gb) {
+    if (threadIdx.x == 0) L.work_to = base_work;
+    base_body<W, NT>(tb, L, seqs, B, n, tag, ws, blockIdx.x, epoch);
+  } else {
+    validate_body<W, NT, true>(tb, L, seqs, B, n, cseq, cpos, ctok, C, verdict, ws, blockIdx.x - gb,
+                               gridDim.x - gb, epoch);
   }
 }
 
@@ -889,6 +969,7 @@ struct epic_ctx {
   int base_slots = 0;
   size_t off_snap = 0, snap_bytes = 0, off_spec = 0, off_bseq = 0;
   uint64_t tag = 0;  // owner tag of the base records this context writes
+  uint32_t epoch = 0;  // launches of base and candidate walks together (walk-record progress words)
   void* scratch = nullptr;  // this device's static scratch (epic_validate_batch_noalloc)
   // witness workspace layout, per sequence (epic_witness)
   size_t wit_stride = 0, wit_rec = 0, wit_mark = 0, wit_stack = 0, wit_w = 0, wit_recs = 0, wit_vis = 0;
@@ -1156,10 +1237,12 @@ epic_status ValidateLaunch<W>::run(epic_ctx* c, const int32_t* seqs, int B, int 
     // candidate's masked run is its sequence's, walked by a base walk
     // (prefix sharing; long sequences also walk their cover graphs, which
     // the selection then reuses)
-    launch_base<W>(c, seqs, B, n, n >= kShareSelectLen ? 2 * B : B, wa, stream);
+    // base walks and candidate walks in one launch (base_validate_kernel)
+    const int gb = n >= kShareSelectLen ? 2 * B : B;
+    if (++c->epoch == 0) ++c->epoch;  // 0 means "no waiting"
     KernelTimer kt(c, kKValidate, stream);
-    hipLaunchKernelGGL((validate_kernel<W, kThreads, true>), dim3(grid), dim3(kThreads), 0, stream, tb, seqs, B, n, cs,
-                       cp, ct, C, verdict, wa);
+    hipLaunchKernelGGL((base_validate_kernel<W, kThreads>), dim3(gb + grid), dim3(kThreads), 0, stream, tb, seqs, B,
+                       n, c->tag, gb, cs, cp, ct, C, verdict, wa, c->epoch, tab_for(c, kKBase).work);
   } else if (W >= 16 && grid <= c->num_cus) {
     KernelTimer kt(c, kKValidate, stream);
     hipLaunchKernelGGL((validate_kernel<W, kThreadsWide, false>), dim3(grid), dim3(kThreadsWide), 0, stream, tb, seqs,
