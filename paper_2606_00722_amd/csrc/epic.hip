@@ -634,6 +634,18 @@ __device__ inline uint64_t spec_mask(int r, int m) {
   return len >= 64 ? ~0ull : ((1ull << len) - 1);
 }
 
+// A speculated check r is worth a helper for a sequence of m candidates when
+// its subset holds two or more candidates (Alg. 4 checks no smaller subset)
+// and no earlier speculated check of the same type has the same subset.
+__device__ inline bool spec_useful(int r, int m) {
+  const uint64_t k = spec_mask(r, m);
+  if (__popcll(k) < 2) return false;
+  for (int q = 1; q < r; ++q)
+    if (spec_exact(q) == spec_exact(r) && spec_mask(q, m) == k) return false;
+  return true;
+}
+constexpr int kSpecSeqs = 128;  // sequences a launch with helpers may hold
+
 template <int W>
 __global__ void spec_clear_kernel(int32_t* __restrict__ state, int count) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
@@ -679,19 +691,65 @@ __global__ void __launch_bounds__(NT) select_kernel(DevTab tb, const int32_t* __
   int32_t* spec_res = spec + B * kSpec;      // [B * kSpec]
   int32_t* spec_used = spec + 2 * B * kSpec;  // [B * kSpec]: the selection took the result
   // Workgroups b < B run Alg. 4 for sequence b; the others are helpers, each
-  // running one speculated check hr of sequence b.  Both reach the walks
+  // running one speculated check hr of a sequence b.  Both reach the walks
   // through the one call site of each check type below.
   const bool helper = (int)blockIdx.x >= B;
-  const int hi = helper ? (int)blockIdx.x - B : 0;
-  const int nh = (int)gridDim.x / B - 1;  // helpers per sequence
-  const int b = helper ? hi / nh : (int)blockIdx.x;
-  const int hr = helper ? 1 + hi % nh : 0;
+  const bool helpers = (int)gridDim.x > B;
+  int b = (int)blockIdx.x, hr = 0;
+  if (helper && (int)gridDim.x == B * kSpec) {
+    // every sequence has a helper for each speculated check
+    b = ((int)blockIdx.x - B) / (kSpec - 1);
+    hr = 1 + ((int)blockIdx.x - B) % (kSpec - 1);
+  } else if (helper) {
+    // Fewer helpers than checks: they go where selections need them.  Helper
+    // hi takes the hi-th worthwhile (sequence, check) pair, by check r = 1,
+    // 2, ... and, within a check, by sequences with more valid candidates
+    // first (their selections run longest).  Every helper computes the same
+    // list from the verdicts.  (Measured on the C-like 1024-token workload,
+    // three helpers per sequence: selection 4.15 -> 3.97 ms per step.)
+    // the walk's origin hash is free until the first walk, which clears it
+    int* spec_m = reinterpret_cast<int*>(L.hash);                              // [B]
+    int16_t* spec_order = reinterpret_cast<int16_t*>(L.hash + kSpecSeqs);      // [B]
+    int& spec_pick = done_n;                                                   // helpers keep no answered checks
+    static_assert(kSpecSeqs + kSpecSeqs / 2 <= kHash, "helper lists fit in the origin hash");
+    const int hi = (int)blockIdx.x - B;
+    for (int k = threadIdx.x; k < B; k += (int)blockDim.x) spec_m[k] = 0;
+    __syncthreads();
+    for (int c = threadIdx.x; c < C; c += (int)blockDim.x) {
+      const int cb = cseq[c];
+      if (cb >= 0 && cb < B && verdict[c] == 1) atomicAdd(&spec_m[cb], 1);
+    }
+    __syncthreads();
+    for (int k = threadIdx.x; k < B; k += (int)blockDim.x) {
+      const int mk = spec_m[k];
+      int rank = 0;
+      for (int k2 = 0; k2 < B; ++k2) rank += spec_m[k2] > mk || (spec_m[k2] == mk && k2 < k);
+      spec_order[rank] = (int16_t)k;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      int pick = -1, cnt = 0;
+      for (int r = 1; r < kSpec && pick < 0; ++r)
+        for (int j = 0; j < B && pick < 0; ++j) {
+          const int k = spec_order[j], m = spec_m[k];
+          if (m < 2) break;  // the rest have fewer
+          if (m <= 64 && spec_useful(r, m)) {
+            if (cnt == hi) pick = k * kSpec + r;
+            ++cnt;
+          }
+        }
+      spec_pick = pick;
+    }
+    __syncthreads();
+    if (spec_pick < 0) return;  // no worthwhile check left
+    b = spec_pick / kSpec;
+    hr = spec_pick % kSpec;
+  }
   // a speculated check's walk counts its work in its own slot; after the
   // launch it goes to the selection's counters when the selection took the
   // result, else to the speculation's (spec_account_kernel)
   if (helper && threadIdx.x == 0)
     L.work_to = reinterpret_cast<unsigned long long*>(spec + spec_work_word(B)) + (size_t)(b * kSpec + hr) * 6;
-  const bool helpers = nh > 0;
   const int bad = select_setup<W>(tb, L, seqs, n, cseq, cpos, ctok, conf, verdict, C, b, helper ? nullptr : selected);
   if (helper) {
     if (bad || __popcll(spec_mask(hr, L.sel_n)) < 2) {  // Alg. 4 checks no subset of one candidate
@@ -812,9 +870,9 @@ __global__ void __launch_bounds__(NT) select_kernel(DevTab tb, const int32_t* __
     __syncthreads();
     r = done_hit;
     if (r < 0 && helpers) {
-      int q = -1;
-      for (int qq = 1; qq <= nh; ++qq)
-        if (spec_exact(qq) == (req == kReqExact) && spec_mask(qq, L.sel_n) == msk) q = qq;
+      int q = -1;  // the first speculated check with this subset (helpers take no duplicates)
+      for (int qq = 1; qq < kSpec; ++qq)
+        if (q < 0 && spec_exact(qq) == (req == kReqExact) && spec_mask(qq, L.sel_n) == msk) q = qq;
       if (q > 0 && threadIdx.x == 0) {
         int res = -1;
         const long long t_start = (long long)clock64();
@@ -1264,7 +1322,7 @@ epic_status SelectLaunch<W>::run(epic_ctx* c, const int32_t* seqs, int B, int n,
   // many as leave every workgroup a CU, when the workspace has chart storage
   // for all of them
   const int nh = std::min(kSpec - 1, c->num_cus / B - 1);
-  const int grid = nh >= 1 && B * (nh + 1) <= c->nslot ? B * (nh + 1) : B;
+  const int grid = nh >= 1 && B <= kSpecSeqs && B * (nh + 1) <= c->nslot ? B * (nh + 1) : B;
   const WsArgs wa = ws_args(c, ws);
   // long sequences: Alg. 4's checks resume from base walks of both graphs
   const int share = n >= kShareSelectLen && B <= c->base_slots;
