@@ -614,13 +614,20 @@ EPIC_INLINE int select_walk(const DevTab& tb, Lds<W>& L, const WgWork& wk, const
 // publish each result with a state word (0 not started, 1 running, 2 done,
 // 3 not applicable).  The selection takes a result that is done, waits for
 // one that is running (its helper is resident and finishes on its own), and
-// otherwise walks the check itself.  Checks, on prefixes of the m candidates
-// sorted by confidence (h = ceil(m/2), the high-confidence half): r = 1 exact
-// on all; 2 relaxed (cover) on h; 3 exact on h; then the next exact checks of
-// ExactShrink's search when the exact check on all fails: 4 on
-// h + ceil((m-h)/2) (the half passed), 5 on ceil(h/2) (it failed).  A
-// launch runs as many of them per sequence as the CUs hold.
-constexpr int kSpec = 6;  // state slots per sequence: slot 0 unused, checks 1..5
+// otherwise walks the check itself.  The checks are on prefixes of the m
+// candidates sorted by confidence (h = ceil(m/2), the high-confidence half):
+// r = 1 exact on all; 2 relaxed (cover) on h; r >= 3 exact on the prefixes
+// ExactShrink's bisection reaches: after the exact check of the prefix that
+// ends an interval [a, b) fails, the interval splits at
+// mid = a + ceil((b-a)/2) and the prefix of mid candidates is checked next.
+// They are numbered breadth-first over the intervals from [0, m), the right
+// interval of each split first (the path on which checks pass), each prefix
+// of two or more candidates once: h, h + ceil((m-h)/2), ceil(h/2), ...  A
+// launch runs as many of them as the CUs hold.
+constexpr int kSpec = 16;  // state slots per sequence: slot 0 unused, checks 1..15
+// Helpers per sequence at most: more (up to 15 at 16 sequences) made every
+// walk of the launch slower (C-like 256-token selection 29.8 -> 31.3 ms).
+constexpr int kSpecHelpers = 5;
 // Speculation block of a selection launch over B sequences (int32 words):
 // state [B*kSpec], result [B*kSpec], consulted flag [B*kSpec], then the work
 // counters of each speculated check's walk (uint64 [B*kSpec][6]).
@@ -628,22 +635,58 @@ constexpr int spec_work_word(int B) { return (3 * B * kSpec + 1) & ~1; }
 constexpr int spec_words(int B) { return spec_work_word(B) + 2 * 6 * B * kSpec; }
 constexpr long long kSpecWaitCycles = 4ll << 30;  // give up waiting on a helper after this many clocks
 __device__ inline bool spec_exact(int r) { return r != 2; }
+
+// Breadth-first bisection of [0, m): calls f(mid) for the split point of each
+// interval of two or more candidates (split points of at least 2), in the
+// order above, until f returns true.
+template <class F>
+__device__ inline void spec_bisect(int m, F f) {
+  for (int d = 0; d < 7; ++d)                  // m <= 64: six levels of halving
+    for (int p = (1 << d) - 1; p >= 0; --p) {  // the right interval first
+      int a = 0, b = m;
+      for (int i = d - 1; i >= 0; --i) {
+        const int mid = a + (b - a + 1) / 2;
+        if ((p >> i) & 1)
+          a = mid;
+        else
+          b = mid;
+      }
+      const int mid = a + (b - a + 1) / 2;
+      if (b - a >= 2 && mid >= 2 && f(mid)) return;
+    }
+}
+
+// Prefix length of speculated check r for m candidates; 0 if there is none.
+__device__ inline int spec_len(int r, int m) {
+  if (r == 1) return m;
+  if (r == 2) return (m + 1) / 2;
+  int k = r - 3, len = 0;
+  spec_bisect(m, [&](int mid) {
+    if (k-- > 0) return false;
+    len = mid;
+    return true;
+  });
+  return len;
+}
+
 __device__ inline uint64_t spec_mask(int r, int m) {
-  const int h = (m + 1) / 2;
-  const int len = r < 2 ? m : r == 4 ? h + (m - h + 1) / 2 : r == 5 ? (h + 1) / 2 : h;
+  const int len = spec_len(r, m);
   return len >= 64 ? ~0ull : ((1ull << len) - 1);
 }
 
-// A speculated check r is worth a helper for a sequence of m candidates when
-// its subset holds two or more candidates (Alg. 4 checks no smaller subset)
-// and no earlier speculated check of the same type has the same subset.
-__device__ inline bool spec_useful(int r, int m) {
-  const uint64_t k = spec_mask(r, m);
-  if (__popcll(k) < 2) return false;
-  for (int q = 1; q < r; ++q)
-    if (spec_exact(q) == spec_exact(r) && spec_mask(q, m) == k) return false;
-  return true;
+// The speculated check of a sequence with m candidates that checks the first
+// len candidates (exactly, or relaxed); 0 if none.
+__device__ inline int spec_find(int m, int len, bool exact) {
+  if (!exact) return len == (m + 1) / 2 ? 2 : 0;
+  if (len == m) return 1;
+  int r = 3, found = 0;
+  spec_bisect(m, [&](int mid) {
+    if (mid == len) found = r;
+    return found != 0 || ++r >= kSpec;
+  });
+  return found;
 }
+
 constexpr int kSpecSeqs = 128;  // sequences a launch with helpers may hold
 
 template <int W>
@@ -696,24 +739,28 @@ __global__ void __launch_bounds__(NT) select_kernel(DevTab tb, const int32_t* __
   const bool helper = (int)blockIdx.x >= B;
   const bool helpers = (int)gridDim.x > B;
   int b = (int)blockIdx.x, hr = 0;
-  if (helper && (int)gridDim.x == B * kSpec) {
-    // every sequence has a helper for each speculated check
-    b = ((int)blockIdx.x - B) / (kSpec - 1);
-    hr = 1 + ((int)blockIdx.x - B) % (kSpec - 1);
-  } else if (helper) {
-    // Fewer helpers than checks: they go where selections need them.  Helper
-    // hi takes the hi-th worthwhile (sequence, check) pair, by check r = 1,
-    // 2, ... and, within a check, by sequences with more valid candidates
-    // first (their selections run longest).  Every helper computes the same
-    // list from the verdicts.  (Measured on the C-like 1024-token workload,
-    // three helpers per sequence: selection 4.15 -> 3.97 ms per step.)
-    // the walk's origin hash is free until the first walk, which clears it
-    int* spec_m = reinterpret_cast<int*>(L.hash);                              // [B]
-    int16_t* spec_order = reinterpret_cast<int16_t*>(L.hash + kSpecSeqs);      // [B]
-    int& spec_pick = done_n;                                                   // helpers keep no answered checks
-    static_assert(kSpecSeqs + kSpecSeqs / 2 <= kHash, "helper lists fit in the origin hash");
+  if (helper) {
+    // Helpers go where selections need them.  Helper hi takes the hi-th
+    // worthwhile (sequence, check) pair, by check r = 1, 2, ... and, within a
+    // check, by sequences with more valid candidates first (their selections
+    // run longest).  Every helper computes the same list from the verdicts.
+    // Measured on the C-like 1024-token workload (three helpers per
+    // sequence): selection 4.15 ms per step with helpers fixed to checks 1-3
+    // of every sequence, 3.92 with these pairs over checks 1-5, 3.58 over
+    // checks 1-15.
+    // The walk's origin hash is free until the first walk, which clears it.
+    int* spec_m = reinterpret_cast<int*>(L.hash);                                  // [B]: valid candidates
+    int16_t* spec_order = reinterpret_cast<int16_t*>(L.hash + kSpecSeqs);          // [B]: by descending count
+    int* spec_nmid = reinterpret_cast<int*>(L.hash + kSpecSeqs + kSpecSeqs / 2);   // [65]: checks r >= 3 for m
+    int& spec_pick = done_n;                                                       // helpers keep no answered checks
+    static_assert(kSpecSeqs + kSpecSeqs / 2 + 65 <= kHash, "helper lists fit in the origin hash");
     const int hi = (int)blockIdx.x - B;
     for (int k = threadIdx.x; k < B; k += (int)blockDim.x) spec_m[k] = 0;
+    for (int mm = threadIdx.x; mm <= 64; mm += (int)blockDim.x) {
+      int cnt = 0;
+      spec_bisect(mm, [&](int) { return ++cnt >= kSpec - 3; });
+      spec_nmid[mm] = cnt;
+    }
     __syncthreads();
     for (int c = threadIdx.x; c < C; c += (int)blockDim.x) {
       const int cb = cseq[c];
@@ -733,7 +780,7 @@ __global__ void __launch_bounds__(NT) select_kernel(DevTab tb, const int32_t* __
         for (int j = 0; j < B && pick < 0; ++j) {
           const int k = spec_order[j], m = spec_m[k];
           if (m < 2) break;  // the rest have fewer
-          if (m <= 64 && spec_useful(r, m)) {
+          if (m <= 64 && (r == 1 || (r == 2 ? m >= 3 : r - 3 < spec_nmid[m]))) {  // check r has 2+ candidates
             if (cnt == hi) pick = k * kSpec + r;
             ++cnt;
           }
@@ -870,9 +917,8 @@ __global__ void __launch_bounds__(NT) select_kernel(DevTab tb, const int32_t* __
     __syncthreads();
     r = done_hit;
     if (r < 0 && helpers) {
-      int q = -1;  // the first speculated check with this subset (helpers take no duplicates)
-      for (int qq = 1; qq < kSpec; ++qq)
-        if (q < 0 && spec_exact(qq) == (req == kReqExact) && spec_mask(qq, L.sel_n) == msk) q = qq;
+      // the speculated check of this subset, if any (they are all prefixes)
+      const int q = (msk & (msk + 1)) == 0 ? spec_find(L.sel_n, __popcll(msk), req == kReqExact) : 0;
       if (q > 0 && threadIdx.x == 0) {
         int res = -1;
         const long long t_start = (long long)clock64();
@@ -1318,11 +1364,10 @@ epic_status SelectLaunch<W>::run(epic_ctx* c, const int32_t* seqs, int B, int n,
                                  const int32_t* cp, const int32_t* ct, const float* conf, const uint8_t* verdict,
                                  int C, uint8_t* sel, int64_t* counts, void* ws, hipStream_t stream) {
   int32_t* spec = (int32_t*)((char*)ws + c->off_spec);
-  // B selection workgroups, then up to kSpec - 1 helpers per sequence, as
-  // many as leave every workgroup a CU, when the workspace has chart storage
-  // for all of them
-  const int nh = std::min(kSpec - 1, c->num_cus / B - 1);
-  const int grid = nh >= 1 && B <= kSpecSeqs && B * (nh + 1) <= c->nslot ? B * (nh + 1) : B;
+  // B selection workgroups, then up to kSpecHelpers helpers per sequence,
+  // as many as leave every workgroup a CU and a chart slot
+  const int nh = std::min({kSpecHelpers, c->num_cus / B - 1, c->nslot / B - 1});
+  const int grid = nh >= 1 && B <= kSpecSeqs ? B * (nh + 1) : B;
   const WsArgs wa = ws_args(c, ws);
   // long sequences: Alg. 4's checks resume from base walks of both graphs
   const int share = n >= kShareSelectLen && B <= c->base_slots;
