@@ -1112,7 +1112,7 @@ epic_status upload(epic_ctx* c) {
          o_lhs = place(blob, H.item_lhs), o_nsym = place(blob, H.next_sym), o_mn = place(blob, H.mn),
          o_gtm = place(blob, H.gap_tm), o_gown = place(blob, H.gap_own), o_ccl = place(blob, H.cover_cl),
          o_enib = place(blob, H.expn_nib), o_pnib = place(blob, H.pred_nib), o_gcov = place(blob, H.gap_cover),
-         o_lnib = place(blob, H.lhs_nib), o_snib = place(blob, H.sym_nib),
+         o_lnib = place(blob, H.lhs_nib), o_snib = place(blob, H.sym_nib), o_psnib = place(blob, H.predsym_nib),
          o_vb = place(blob, H.vbytes), o_vo = place(blob, H.voffs), o_endof = place(blob, H.end_of),
          o_dot0 = place(blob, H.dot0), o_wynt = place(blob, H.wy_nt), o_wyown = place(blob, H.wy_own),
          o_wypool = place(blob, H.wy_pool);
@@ -1178,6 +1178,7 @@ epic_status upload(epic_ctx* c) {
   t.gap_cover = (const uint32_t*)(d + o_gcov);
   t.lhs_nib = (const uint64_t*)(d + o_lnib);
   t.sym_nib = (const uint64_t*)(d + o_snib);
+  t.predsym_nib = (const uint64_t*)(d + o_psnib);
   t.cover_cl = (const uint32_t*)(d + o_ccl);
   t.vbytes = (const uint8_t*)(d + o_vb);
   t.voffs = (const int32_t*)(d + o_vo);

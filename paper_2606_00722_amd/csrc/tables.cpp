@@ -477,6 +477,16 @@ int build_tables(int Q, const int16_t* trans, const int16_t* accept, int T, int 
           else if (sym >= 0)
             H.sym_nib[2 * e + 1] |= 1ull << sym;
         }
+  H.predsym_nib.assign((size_t)16 * 16 * 2, 0);
+  for (int e = 0; e < 16 * 16; ++e)
+    for (int w = 0; w < W; ++w)
+      for (uint32_t bits = H.pred_nib[(size_t)e * W + w]; bits; bits &= bits - 1) {
+        const int sym = H.next_sym[w * 32 + __builtin_ctz(bits)];
+        if (sym >= 64)
+          H.predsym_nib[2 * e] |= 1ull << (sym - 64);
+        else if (sym >= 0)
+          H.predsym_nib[2 * e + 1] |= 1ull << sym;
+      }
 
   // ---------------------------------------------------------------- cover
   {

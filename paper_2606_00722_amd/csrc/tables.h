@@ -55,6 +55,9 @@ struct HostTables {
   // nonterminals and terminals its items expect (sym_nib: pairs of words)
   std::vector<uint64_t> lhs_nib;  // [W*8*16]
   std::vector<uint64_t> sym_nib;  // [W*8*16*2]
+  // the nonterminals and terminals expected by the items of pred_nib's entry
+  // (i, v), pairs of words: the symbols a prediction closure expects
+  std::vector<uint64_t> predsym_nib;  // [16*16*2]
   std::vector<uint32_t> start_of;  // [N*W] items A -> . gamma
   std::vector<uint32_t> end_of;    // [N*W] items A -> gamma .
   // regular cover: state bit i < 32W is dotted item i (rule position), bit 32W+A is
