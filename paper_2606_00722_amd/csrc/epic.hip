@@ -16,9 +16,12 @@
 
 #include <algorithm>
 #include <atomic>
+#include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <memory>
 #include <mutex>
+#include <queue>
 #include <random>
 #include <string>
 #include <vector>
@@ -294,7 +297,9 @@ __device__ inline uint64_t wait_record(const char* snap, uint32_t epoch, int run
   const uint64_t* p = reinterpret_cast<const uint64_t*>(snap + 24);
   const long long t_start = (long long)clock64();
   for (;;) {
-    const uint64_t v = __hip_atomic_load(p, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
+    // relaxed: an acquire load on every poll would invalidate this XCD's L2
+    // under every walk resident there; the caller fences once it returns
+    const uint64_t v = __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const uint32_t st = (uint32_t)v;
     if ((uint32_t)(v >> 32) == epoch && ((st & kRecDone) || (int)st > run)) return v;
     if ((long long)clock64() - t_start > kRecWaitCycles) return 0;
@@ -428,6 +433,7 @@ __global__ void __launch_bounds__(NT) base_validate_kernel(DevTab tb, const int3
 // ------------------------------------------------------------------ select
 // Alg. 4 as a stack machine run by thread 0; checks are walks by the whole
 // workgroup.  Subsets are bit masks over the confidence-sorted candidates.
+// The host runs the same machine to plan speculated checks.
 enum : int { kRS = 0, kES = 1, kTop = 2 };
 enum : int { kReqNone = 0, kReqCover = 1, kReqExact = 2, kReqDone = 3 };
 
@@ -436,8 +442,10 @@ struct Frame {
   uint64_t A, S, t1;
 };
 
-__device__ inline void split_halves(uint64_t S, uint64_t& lo, uint64_t& hi) {
-  int cnt = __popcll(S), h = (cnt + 1) / 2;  // ceil(|S|/2) on the high-confidence side
+__host__ __device__ inline int popc64(uint64_t x) { return __builtin_popcountll(x); }
+
+__host__ __device__ inline void split_halves(uint64_t S, uint64_t& lo, uint64_t& hi) {
+  int cnt = popc64(S), h = (cnt + 1) / 2;  // ceil(|S|/2) on the high-confidence side
   lo = 0;
   uint64_t s = S;
   for (int i = 0; i < h; ++i) {
@@ -446,6 +454,136 @@ __device__ inline void split_halves(uint64_t S, uint64_t& lo, uint64_t& hi) {
     s &= s - 1;
   }
   hi = S & ~lo;
+}
+
+// ExactShrink(x, RelaxedSelect(x, C)) over the m sorted candidates: advance()
+// runs until the machine asks a check (req = kReqCover or kReqExact on
+// `mask`) or finishes (req = kReqDone, the selection in final_B); the caller
+// puts the check's outcome in res before the next advance().
+struct Alg4 {
+  Frame stack[96];  // depth <= 2 + 3 * log2(64) frames
+  int sp, req, res;
+  uint64_t mask, ret_val, final_B;
+};
+
+__host__ __device__ inline void alg4_start(Alg4& a, int m) {
+  a.stack[0] = Frame{kTop, 0, 0, m >= 64 ? ~0ull : ((1ull << m) - 1), 0};
+  a.sp = 1;
+  a.req = kReqNone;
+  a.res = 0;
+  a.mask = 0;
+  a.ret_val = 0;
+  a.final_B = 0;
+}
+
+__host__ __device__ inline void alg4_advance(Alg4& a) {
+  a.req = kReqNone;
+  while (a.req == kReqNone) {
+    if (a.sp == 0 || a.sp >= 95) {  // >= 95 cannot happen for <= 64 candidates
+      a.req = kReqDone;
+      break;
+    }
+    Frame& f = a.stack[a.sp - 1];
+    if (f.type == kTop) {
+      if (f.stage == 0) {
+        f.stage = 1;
+        a.stack[a.sp++] = Frame{kRS, 0, 0, f.S, 0};
+      } else if (f.stage == 1) {
+        f.stage = 2;
+        a.stack[a.sp++] = Frame{kES, 0, 0, a.ret_val, 0};
+      } else {
+        a.final_B = a.ret_val;
+        --a.sp;
+      }
+      continue;
+    }
+    const bool is_rs = f.type == kRS;
+    if (f.stage == 0) {
+      if (popc64(f.S) <= 1) {
+        a.ret_val = 0;
+        --a.sp;
+        continue;
+      }
+      f.stage = 1;
+      a.req = is_rs ? kReqCover : kReqExact;
+      a.mask = f.A | f.S;
+      break;
+    }
+    if (f.stage == 1) {
+      if (a.res) {
+        a.ret_val = f.S;
+        --a.sp;
+        continue;
+      }
+      uint64_t lo, hi;
+      split_halves(f.S, lo, hi);
+      f.stage = 2;
+      a.stack[a.sp++] = Frame{is_rs ? kRS : kES, 0, f.A, lo, 0};
+      continue;
+    }
+    if (f.stage == 2) {
+      uint64_t lo, hi;
+      split_halves(f.S, lo, hi);
+      f.t1 = a.ret_val;  // B_L (RelaxedSelect) or B'_L (ExactShrink)
+      f.stage = 3;
+      a.stack[a.sp++] = Frame{kRS, 0, f.A | f.t1, hi, 0};
+      continue;
+    }
+    if (f.stage == 3) {
+      if (is_rs) {
+        a.ret_val = f.t1 | a.ret_val;
+        --a.sp;
+        continue;
+      }
+      f.stage = 4;  // B'_R = ret_val; now ExactShrink(x + B'_L, B'_R)
+      a.stack[a.sp++] = Frame{kES, 0, f.A | f.t1, a.ret_val, 0};
+      continue;
+    }
+    // ExactShrink stage 4: B''_R = ret_val
+    a.ret_val = f.t1 | a.ret_val;
+    --a.sp;
+  }
+}
+
+// Answered checks: Alg. 4 asks some again (after an exact check fails and a
+// half passes, the next RelaxedSelect and ExactShrink repeat the cover and
+// exact checks of the whole set).  The selection remembers the first
+// kDoneChecks answers of a sequence; a check found here is not walked.
+__host__ __device__ inline int done_find(const uint64_t* msk, const int* val, int n, uint64_t m, int kind) {
+  int hit = -1;
+  for (int k = 0; k < n; ++k)
+    if (msk[k] == m && (val[k] & 2) == kind) hit = val[k] & 1;
+  return hit;
+}
+
+// Replays the machine from its start along a path of outcomes (bit i: the
+// outcome of the i-th check not found in the answered checks) until the
+// check at depth d; false when the machine finishes first.  On true, a.req
+// and a.mask are that check.
+__host__ __device__ inline bool alg4_replay(Alg4& a, int m, uint64_t path, int d, uint64_t* dmsk, int* dval, int& dn) {
+  alg4_start(a, m);
+  dn = 0;
+  int depth = 0;
+  for (int guard = 0; guard < 1 << 16; ++guard) {
+    alg4_advance(a);
+    if (a.req == kReqDone) return false;
+    const int kind = a.req == kReqCover ? 2 : 0;
+    const int hit = done_find(dmsk, dval, dn, a.mask, kind);
+    if (hit >= 0) {
+      a.res = hit;
+      continue;
+    }
+    if (depth == d) return true;
+    const int r = (int)((path >> depth) & 1);
+    ++depth;
+    if (dn < kDoneChecks) {
+      dmsk[dn] = a.mask;
+      dval[dn] = r | kind;
+      ++dn;
+    }
+    a.res = r;
+  }
+  return false;
 }
 
 // The candidates Alg. 4 selects from for sequence b: its verdict-1
@@ -608,86 +746,55 @@ EPIC_INLINE int select_walk(const DevTab& tb, Lds<W>& L, const WgWork& wk, const
     return select_walk_body<W, COVER, SHARE>(tb, L, wk, ws, seqs, n, b, msk);
 }
 
-// Speculated checks: besides its first check (relaxed, on all candidates),
-// the checks Alg. 4 asks for next in the common cases are known before it
-// runs.  Helper workgroups walk them concurrently with the selection and
-// publish each result with a state word (0 not started, 1 running, 2 done,
-// 3 not applicable).  The selection takes a result that is done, waits for
-// one that is running (its helper is resident and finishes on its own), and
-// otherwise walks the check itself.  The checks are on prefixes of the m
-// candidates sorted by confidence (h = ceil(m/2), the high-confidence half):
-// r = 1 exact on all; 2 relaxed (cover) on h; r >= 3 exact on the prefixes
-// ExactShrink's bisection reaches: after the exact check of the prefix that
-// ends an interval [a, b) fails, the interval splits at
-// mid = a + ceil((b-a)/2) and the prefix of mid candidates is checked next.
-// They are numbered breadth-first over the intervals from [0, m), the right
-// interval of each split first (the path on which checks pass), each prefix
-// of two or more candidates once: h, h + ceil((m-h)/2), ceil(h/2), ...  A
-// launch runs as many of them as the CUs hold.
-constexpr int kSpec = 16;  // state slots per sequence: slot 0 unused, checks 1..15
+// Speculated checks.  The machine's next check depends only on the number m
+// of candidates and on the outcomes of the checks it has made, so its checks
+// form one binary decision tree per m.  A node is a path of outcomes: those
+// of the checks before it that were not found among the answered checks.
+// The root, the relaxed check of all candidates, is the selection's own
+// first walk.  For every m the host lists the nodes below the root by
+// decreasing estimated probability (outcomes taken as independent, a
+// relaxed check passing with probability 0.62, an exact one with 0.79), at
+// most kPlan of them, each with a level: twice the negative base-2
+// logarithm of that probability, rounded down.  Helper workgroups take
+// (sequence, node) pairs level by level, sequence by sequence within a
+// level.  A helper replays the machine along its node's path to learn the
+// node's check (or that the machine finishes before it), walks it and
+// publishes the result with a state word (0 not started, 1 running, 2 done,
+// 3 no check there).  The selection looks up the node of its own path: it
+// takes a result that is done, waits for one that is running (its helper
+// is resident and finishes on its own), and otherwise walks the check
+// itself.  The plan decides only which checks run early: a helper's result
+// is that of the check the machine asks at its node.
+constexpr int kPlan = 64;        // planned nodes (state slots) per sequence
+constexpr int kPlanLevels = 32;  // levels of the helper order
+constexpr double kPlanPassRelaxed = 0.62, kPlanPassExact = 0.79;
+// Plan table (int32 words): level starts [65][kPlanLevels + 1] (the nodes of
+// m at level l are kPlan*m + start[l] .. start[l+1]-1; start[kPlanLevels] is
+// their count), then the nodes [65][kPlan] as {depth, level, path low word,
+// path high word}.
+constexpr int kPlanNodeWord = 65 * (kPlanLevels + 1);
+constexpr int kPlanWords = kPlanNodeWord + 65 * kPlan * 4;
 // Helpers per sequence at most: more (up to 15 at 16 sequences) made every
 // walk of the launch slower (C-like 256-token selection 29.8 -> 31.3 ms).
 constexpr int kSpecHelpers = 5;
 // Speculation block of a selection launch over B sequences (int32 words):
-// state [B*kSpec], result [B*kSpec], consulted flag [B*kSpec], then the work
-// counters of each speculated check's walk (uint64 [B*kSpec][6]).
-constexpr int spec_work_word(int B) { return (3 * B * kSpec + 1) & ~1; }
-constexpr int spec_words(int B) { return spec_work_word(B) + 2 * 6 * B * kSpec; }
+// state [B*kPlan], result [B*kPlan], consulted flag [B*kPlan], then the work
+// counters of each speculated check's walk (uint64 [B*kPlan][6]).
+constexpr int spec_work_word(int B) { return (3 * B * kPlan + 1) & ~1; }
+constexpr int spec_words(int B) { return spec_work_word(B) + 2 * 6 * B * kPlan; }
 constexpr long long kSpecWaitCycles = 4ll << 30;  // give up waiting on a helper after this many clocks
-__device__ inline bool spec_exact(int r) { return r != 2; }
-
-// Breadth-first bisection of [0, m): calls f(mid) for the split point of each
-// interval of two or more candidates (split points of at least 2), in the
-// order above, until f returns true.
-template <class F>
-__device__ inline void spec_bisect(int m, F f) {
-  for (int d = 0; d < 7; ++d)                  // m <= 64: six levels of halving
-    for (int p = (1 << d) - 1; p >= 0; --p) {  // the right interval first
-      int a = 0, b = m;
-      for (int i = d - 1; i >= 0; --i) {
-        const int mid = a + (b - a + 1) / 2;
-        if ((p >> i) & 1)
-          a = mid;
-        else
-          b = mid;
-      }
-      const int mid = a + (b - a + 1) / 2;
-      if (b - a >= 2 && mid >= 2 && f(mid)) return;
-    }
-}
-
-// Prefix length of speculated check r for m candidates; 0 if there is none.
-__device__ inline int spec_len(int r, int m) {
-  if (r == 1) return m;
-  if (r == 2) return (m + 1) / 2;
-  int k = r - 3, len = 0;
-  spec_bisect(m, [&](int mid) {
-    if (k-- > 0) return false;
-    len = mid;
-    return true;
-  });
-  return len;
-}
-
-__device__ inline uint64_t spec_mask(int r, int m) {
-  const int len = spec_len(r, m);
-  return len >= 64 ? ~0ull : ((1ull << len) - 1);
-}
-
-// The speculated check of a sequence with m candidates that checks the first
-// len candidates (exactly, or relaxed); 0 if none.
-__device__ inline int spec_find(int m, int len, bool exact) {
-  if (!exact) return len == (m + 1) / 2 ? 2 : 0;
-  if (len == m) return 1;
-  int r = 3, found = 0;
-  spec_bisect(m, [&](int mid) {
-    if (mid == len) found = r;
-    return found != 0 || ++r >= kSpec;
-  });
-  return found;
-}
-
 constexpr int kSpecSeqs = 128;  // sequences a launch with helpers may hold
+
+// Helpers per sequence at most: its first kPlanUse planned nodes.
+constexpr int kPlanUse = 64;
+
+// Helper pairs at level l of a sequence with m candidates.
+__device__ inline int plan_level_count(const int32_t* plan, int m, int l) {
+  if (m < 2 || m > 64) return 0;
+  const int32_t* st = plan + m * (kPlanLevels + 1);
+  const int a = st[l] < kPlanUse ? st[l] : kPlanUse, b = st[l + 1] < kPlanUse ? st[l + 1] : kPlanUse;
+  return b - a;
+}
 
 template <int W>
 __global__ void spec_clear_kernel(int32_t* __restrict__ state, int count) {
@@ -702,10 +809,10 @@ template <int W>
 __global__ void spec_account_kernel(const int32_t* __restrict__ spec, int B, unsigned long long* used,
                                     unsigned long long* unused) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= B * kSpec) return;
+  if (i >= B * kPlan) return;
   const unsigned long long* w = reinterpret_cast<const unsigned long long*>(spec + spec_work_word(B)) + (size_t)i * 6;
   if (w[0] == 0) return;
-  unsigned long long* to = spec[2 * B * kSpec + i] ? used : unused;
+  unsigned long long* to = spec[2 * B * kPlan + i] ? used : unused;
   for (int k = 0; k < 6; ++k) atomicAdd(&to[k], w[k]);
 }
 
@@ -719,231 +826,161 @@ __global__ void __launch_bounds__(NT) select_kernel(DevTab tb, const int32_t* __
                                                           uint8_t* __restrict__ selected, long long* counts,
                                                           int32_t* __restrict__ spec, WsArgs ws) {
   __shared__ Lds<W> L;
-  __shared__ Frame stack[96];
-  __shared__ int sp;
-  __shared__ uint64_t ret_val, final_B;
-  // checks already answered for this sequence: Alg. 4 asks some again (after
-  // an exact check fails and a half passes, the next RelaxedSelect and
-  // ExactShrink repeat the cover and exact checks of the whole set)
+  __shared__ Alg4 M;
   __shared__ uint64_t done_msk[kDoneChecks];
   __shared__ int done_val[kDoneChecks];  // result | (cover ? 2 : 0)
-  __shared__ int done_n, done_hit;
+  __shared__ int done_n, done_hit, spec_pick, plan_j;
   const WgWork wk = slot_work(ws, blockIdx.x);
   stage_tables<W>(tb, L);
-  int32_t* spec_state = spec;               // [B * kSpec]
-  int32_t* spec_res = spec + B * kSpec;      // [B * kSpec]
-  int32_t* spec_used = spec + 2 * B * kSpec;  // [B * kSpec]: the selection took the result
+  int32_t* spec_state = spec;                 // [B * kPlan]
+  int32_t* spec_res = spec + B * kPlan;       // [B * kPlan]
+  int32_t* spec_used = spec + 2 * B * kPlan;  // [B * kPlan]: the selection took the result
   // Workgroups b < B run Alg. 4 for sequence b; the others are helpers, each
-  // running one speculated check hr of a sequence b.  Both reach the walks
-  // through the one call site of each check type below.
+  // walking the check of one planned node of a sequence b.  Both reach the
+  // walks through the one call site of each check type below.
   const bool helper = (int)blockIdx.x >= B;
   const bool helpers = (int)gridDim.x > B;
-  int b = (int)blockIdx.x, hr = 0;
+  int b = (int)blockIdx.x, hj = 0;
   if (helper) {
-    // Helpers go where selections need them.  Helper hi takes the hi-th
-    // worthwhile (sequence, check) pair, by check r = 1, 2, ... and, within a
-    // check, by sequences with more valid candidates first (their selections
-    // run longest).  Every helper computes the same list from the verdicts.
-    // Measured on the C-like 1024-token workload (three helpers per
-    // sequence): selection 4.15 ms per step with helpers fixed to checks 1-3
-    // of every sequence, 3.92 with these pairs over checks 1-5, 3.58 over
-    // checks 1-15.
-    // The walk's origin hash is free until the first walk, which clears it.
-    int* spec_m = reinterpret_cast<int*>(L.hash);                                  // [B]: valid candidates
-    int16_t* spec_order = reinterpret_cast<int16_t*>(L.hash + kSpecSeqs);          // [B]: by descending count
-    int* spec_nmid = reinterpret_cast<int*>(L.hash + kSpecSeqs + kSpecSeqs / 2);   // [65]: checks r >= 3 for m
-    int& spec_pick = done_n;                                                       // helpers keep no answered checks
-    static_assert(kSpecSeqs + kSpecSeqs / 2 + 65 <= kHash, "helper lists fit in the origin hash");
+    // Helper hi takes the hi-th (sequence, node) pair: by level, then by
+    // sequence, then by the node's place in the sequence's plan.  Every
+    // helper computes the same order from the verdicts: the valid candidates
+    // per sequence, then a prefix sum over the (level, sequence) cells.  The
+    // walk's origin hash is free until the first walk, which clears it.
+    int* spec_m = reinterpret_cast<int*>(L.hash);  // [B]: valid candidates
+    static_assert(kSpecSeqs <= kHash, "helper counts fit in the origin hash");
     const int hi = (int)blockIdx.x - B;
     for (int k = threadIdx.x; k < B; k += (int)blockDim.x) spec_m[k] = 0;
-    for (int mm = threadIdx.x; mm <= 64; mm += (int)blockDim.x) {
-      int cnt = 0;
-      spec_bisect(mm, [&](int) { return ++cnt >= kSpec - 3; });
-      spec_nmid[mm] = cnt;
-    }
+    if (threadIdx.x == 0) spec_pick = -1;
     __syncthreads();
     for (int c = threadIdx.x; c < C; c += (int)blockDim.x) {
       const int cb = cseq[c];
       if (cb >= 0 && cb < B && verdict[c] == 1) atomicAdd(&spec_m[cb], 1);
     }
     __syncthreads();
-    for (int k = threadIdx.x; k < B; k += (int)blockDim.x) {
-      const int mk = spec_m[k];
-      int rank = 0;
-      for (int k2 = 0; k2 < B; ++k2) rank += spec_m[k2] > mk || (spec_m[k2] == mk && k2 < k);
-      spec_order[rank] = (int16_t)k;
-    }
-    __syncthreads();
-    if (threadIdx.x == 0) {
-      int pick = -1, cnt = 0;
-      for (int r = 1; r < kSpec && pick < 0; ++r)
-        for (int j = 0; j < B && pick < 0; ++j) {
-          const int k = spec_order[j], m = spec_m[k];
-          if (m < 2) break;  // the rest have fewer
-          if (m <= 64 && (r == 1 || (r == 2 ? m >= 3 : r - 3 < spec_nmid[m]))) {  // check r has 2+ candidates
-            if (cnt == hi) pick = k * kSpec + r;
-            ++cnt;
-          }
+    const int ncell = kPlanLevels * B, per = (ncell + (int)blockDim.x - 1) / (int)blockDim.x;
+    const int c0 = (int)threadIdx.x * per, c1 = c0 + per < ncell ? c0 + per : ncell;
+    int sum = 0;
+    for (int c = c0; c < c1; ++c) sum += plan_level_count(tb.plan, spec_m[c % B], c / B);
+    int total = 0;
+    int acc = block_scan<W>(L, sum, &total);
+    if (hi >= acc && hi < acc + sum)
+      for (int c = c0; c < c1; ++c) {
+        const int bb = c % B, lvl = c / B, k = plan_level_count(tb.plan, spec_m[bb], lvl);
+        if (hi < acc + k) {
+          spec_pick = bb * kPlan + tb.plan[spec_m[bb] * (kPlanLevels + 1) + lvl] + (hi - acc);
+          break;
         }
-      spec_pick = pick;
-    }
+        acc += k;
+      }
     __syncthreads();
-    if (spec_pick < 0) return;  // no worthwhile check left
-    b = spec_pick / kSpec;
-    hr = spec_pick % kSpec;
+    if (spec_pick < 0) return;  // no planned node left
+    b = spec_pick / kPlan;
+    hj = spec_pick % kPlan;
   }
   // a speculated check's walk counts its work in its own slot; after the
   // launch it goes to the selection's counters when the selection took the
   // result, else to the speculation's (spec_account_kernel)
   if (helper && threadIdx.x == 0)
-    L.work_to = reinterpret_cast<unsigned long long*>(spec + spec_work_word(B)) + (size_t)(b * kSpec + hr) * 6;
+    L.work_to = reinterpret_cast<unsigned long long*>(spec + spec_work_word(B)) + (size_t)(b * kPlan + hj) * 6;
   const int bad = select_setup<W>(tb, L, seqs, n, cseq, cpos, ctok, conf, verdict, C, b, helper ? nullptr : selected);
   if (helper) {
-    if (bad || __popcll(spec_mask(hr, L.sel_n)) < 2) {  // Alg. 4 checks no subset of one candidate
-      if (threadIdx.x == 0) __hip_atomic_store(&spec_state[b * kSpec + hr], 3, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
-      return;
+    if (threadIdx.x == 0) {
+      // the node's check: the machine replayed along the node's path
+      const int m = L.sel_n;
+      bool found = false;
+      if (!bad && m >= 2 && m <= 64 && hj < tb.plan[m * (kPlanLevels + 1) + kPlanLevels]) {
+        const int32_t* e = tb.plan + kPlanNodeWord + (m * kPlan + hj) * 4;
+        const uint64_t path = (uint64_t)(uint32_t)e[2] | ((uint64_t)(uint32_t)e[3] << 32);
+        found = alg4_replay(M, m, path, e[0], done_msk, done_val, done_n);
+      }
+      plan_j = found ? 1 : 0;
+      __hip_atomic_store(&spec_state[b * kPlan + hj], found ? 1 : 3, found ? __ATOMIC_RELAXED : __ATOMIC_RELEASE,
+                         __HIP_MEMORY_SCOPE_AGENT);
     }
-    if (threadIdx.x == 0) __hip_atomic_store(&spec_state[b * kSpec + hr], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __syncthreads();
+    if (!plan_j) return;
   } else if (threadIdx.x == 0) {
-    const int m = L.sel_n;
     if (L.sel_bad)
       atomicOr(tb.dev_err, L.sel_bad == 2   ? (uint32_t)EPIC_DEV_CAPACITY
                            : L.sel_bad == 3 ? (uint32_t)EPIC_DEV_BAD_CANDIDATE
                                             : (uint32_t)EPIC_DEV_BAD_SELECT);
     done_n = 0;
-    sp = 0;
-    stack[0] = Frame{kTop, 0, 0, m >= 64 ? ~0ull : ((1ull << m) - 1), 0};
-    sp = 1;
-    ret_val = 0;
-    final_B = 0;
+    alg4_start(M, L.sel_n);
   }
   __syncthreads();
   if (!helper && L.sel_bad) return;
   long long ncover = 0, nexact = 0;
   bool failed = false;
+  // the path: outcomes of the checks so far that were not answered checks
+  int pdepth = 0;
+  uint64_t pbits = 0;
   for (int step = 0; step < 1 << 20; ++step) {
     int req;
     uint64_t msk;
     int r = -1;
     if (helper) {
-      req = spec_exact(hr) ? kReqExact : kReqCover;
-      msk = spec_mask(hr, L.sel_n);
+      req = M.req;
+      msk = M.mask;
     } else {
-    if (threadIdx.x == 0) {
-      // run the machine until it needs a check or finishes
-      L.sel_req = kReqNone;
-      while (L.sel_req == kReqNone) {
-        if (sp == 0) {
-          L.sel_req = kReqDone;
-          break;
-        }
-        Frame& f = stack[sp - 1];
-        if (f.type == kTop) {
-          if (f.stage == 0) {
-            f.stage = 1;
-            stack[sp++] = Frame{kRS, 0, 0, f.S, 0};
-          } else if (f.stage == 1) {
-            f.stage = 2;
-            stack[sp++] = Frame{kES, 0, 0, ret_val, 0};
-          } else {
-            final_B = ret_val;
-            --sp;
-          }
-          continue;
-        }
-        const bool is_rs = f.type == kRS;
-        if (f.stage == 0) {
-          if (__popcll(f.S) <= 1) {
-            ret_val = 0;
-            --sp;
-            continue;
-          }
-          f.stage = 1;
-          L.sel_req = is_rs ? kReqCover : kReqExact;
-          L.sel_mask = f.A | f.S;
-          break;
-        }
-        if (f.stage == 1) {
-          if (L.sel_res) {
-            ret_val = f.S;
-            --sp;
-            continue;
-          }
-          uint64_t lo, hi;
-          split_halves(f.S, lo, hi);
-          f.stage = 2;
-          stack[sp++] = Frame{is_rs ? kRS : kES, 0, f.A, lo, 0};
-          continue;
-        }
-        if (f.stage == 2) {
-          uint64_t lo, hi;
-          split_halves(f.S, lo, hi);
-          f.t1 = ret_val;  // B_L (RelaxedSelect) or B'_L (ExactShrink)
-          f.stage = 3;
-          stack[sp++] = Frame{kRS, 0, f.A | f.t1, hi, 0};
-          continue;
-        }
-        if (f.stage == 3) {
-          if (is_rs) {
-            ret_val = f.t1 | ret_val;
-            --sp;
-            continue;
-          }
-          f.stage = 4;  // B'_R = ret_val; now ExactShrink(x + B'_L, B'_R)
-          stack[sp++] = Frame{kES, 0, f.A | f.t1, ret_val, 0};
-          continue;
-        }
-        // ExactShrink stage 4: B''_R = ret_val
-        ret_val = f.t1 | ret_val;
-        --sp;
+      if (threadIdx.x == 0) alg4_advance(M);
+      __syncthreads();
+      req = M.req;
+      if (req == kReqDone) break;
+      msk = M.mask;
+      if (req == kReqCover)
+        ++ncover;
+      else
+        ++nexact;
+      const int kind = req == kReqCover ? 2 : 0;
+      if (threadIdx.x == 0) {
+        done_hit = done_find(done_msk, done_val, done_n, msk, kind);
+        plan_j = -1;
       }
-      if (sp >= 95) L.sel_req = kReqDone;  // cannot happen for <= 64 candidates
-    }
-    __syncthreads();
-    req = L.sel_req;
-    if (req == kReqDone) break;
-    msk = L.sel_mask;
-    if (req == kReqCover)
-      ++ncover;
-    else
-      ++nexact;
-    const int kind = req == kReqCover ? 2 : 0;
-    if (threadIdx.x == 0) {
-      int hit = -1;
-      for (int k = 0; k < done_n; ++k)
-        if (done_msk[k] == msk && (done_val[k] & 2) == kind) hit = done_val[k] & 1;
-      done_hit = hit;
-    }
-    __syncthreads();
-    r = done_hit;
-    if (r < 0 && helpers) {
-      // the speculated check of this subset, if any (they are all prefixes)
-      const int q = (msk & (msk + 1)) == 0 ? spec_find(L.sel_n, __popcll(msk), req == kReqExact) : 0;
-      if (q > 0 && threadIdx.x == 0) {
-        int res = -1;
-        const long long t_start = (long long)clock64();
-        while ((long long)clock64() - t_start < kSpecWaitCycles) {
-          const int st = __hip_atomic_load(&spec_state[b * kSpec + q], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
-          if (st == 2) res = spec_res[b * kSpec + q];
-          if (st != 1) break;
-          __builtin_amdgcn_s_sleep(8);
+      __syncthreads();
+      r = done_hit;
+      if (r < 0 && helpers && pdepth >= 1 && pdepth < 64) {
+        // the planned node of this path, if any
+        const int m = L.sel_n;
+        const int cnt = tb.plan[m * (kPlanLevels + 1) + kPlanLevels];
+        for (int j = threadIdx.x; j < cnt; j += (int)blockDim.x) {
+          const int32_t* e = tb.plan + kPlanNodeWord + (m * kPlan + j) * 4;
+          const uint64_t path = (uint64_t)(uint32_t)e[2] | ((uint64_t)(uint32_t)e[3] << 32);
+          if (e[0] == pdepth && path == pbits) plan_j = j;
         }
-        if (res >= 0) spec_used[b * kSpec + q] = 1;
-        L.sel_res = res;
-      }
-      if (q > 0) {
         __syncthreads();
-        r = L.sel_res;
+        const int q = plan_j;
+        if (q >= 0 && threadIdx.x == 0) {
+          int res = -1;
+          const long long t_start = (long long)clock64();
+          while ((long long)clock64() - t_start < kSpecWaitCycles) {
+            // relaxed polls, one acquire fence when the result is there (an
+            // acquire load per poll would invalidate this XCD's L2 each time)
+            const int st = __hip_atomic_load(&spec_state[b * kPlan + q], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (st == 2) {
+              __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+              res = __hip_atomic_load(&spec_res[b * kPlan + q], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+            if (st != 1) break;
+            __builtin_amdgcn_s_sleep(8);
+          }
+          if (res >= 0) spec_used[b * kPlan + q] = 1;
+          L.sel_res = res;
+        }
+        if (q >= 0) {
+          __syncthreads();
+          r = L.sel_res;
+        }
       }
     }
-    }
+    const bool fresh = done_hit < 0;  // not an answered check: the path grows
     if (r < 0)
       r = req == kReqCover ? select_walk<W, true, SHARE>(tb, L, wk, ws, seqs, n, b, msk)
                            : select_walk<W, false, SHARE>(tb, L, wk, ws, seqs, n, b, msk);
     if (helper) {
       if (threadIdx.x == 0) {
-        spec_res[b * kSpec + hr] = r < 0 ? -1 : r;  // capacity: the selection walks it again and reports
-        __hip_atomic_store(&spec_state[b * kSpec + hr], 2, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+        spec_res[b * kPlan + hj] = r < 0 ? -1 : r;  // capacity: the selection walks it again and reports
+        __hip_atomic_store(&spec_state[b * kPlan + hj], 2, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
       }
       return;
     }
@@ -951,9 +988,13 @@ __global__ void __launch_bounds__(NT) select_kernel(DevTab tb, const int32_t* __
       failed = true;
       break;
     }
+    if (fresh) {
+      if (pdepth < 64) pbits |= (uint64_t)r << pdepth;
+      ++pdepth;
+    }
     if (threadIdx.x == 0) {
-      L.sel_res = r;
-      if (done_hit < 0 && done_n < kDoneChecks) {
+      M.res = r;
+      if (fresh && done_n < kDoneChecks) {
         done_msk[done_n] = msk;
         done_val[done_n] = r | (req == kReqCover ? 2 : 0);
         ++done_n;
@@ -970,7 +1011,7 @@ __global__ void __launch_bounds__(NT) select_kernel(DevTab tb, const int32_t* __
       atomicOr(tb.dev_err, (uint32_t)EPIC_DEV_CAPACITY | (1u << (8 + (L.overflow & 15))));
     } else {
       for (int i = 0; i < L.sel_n; ++i)
-        if ((final_B >> i) & 1) selected[L.sel_idx[i]] = 1;
+        if ((M.final_B >> i) & 1) selected[L.sel_idx[i]] = 1;
     }
   }
 }
@@ -1102,6 +1143,59 @@ size_t place(std::vector<char>& blob, const std::vector<T>& v) {
   return off;
 }
 
+// The selection's speculation plan: for m = 2..64 candidates, the nodes of
+// the machine's decision tree below the root by decreasing estimated
+// probability, best first (a node's children are its check's two outcomes),
+// in the layout of kPlanWords.  The same for every context.
+const std::vector<int32_t>& speculation_plan() {
+  static const std::vector<int32_t> plan = [] {
+    std::vector<int32_t> pl(kPlanWords, 0);
+    struct Node {
+      double nl;  // -log2 of the estimated probability
+      uint64_t path;
+      int depth;
+    };
+    auto later = [](const Node& x, const Node& y) {
+      if (x.nl != y.nl) return x.nl > y.nl;
+      if (x.depth != y.depth) return x.depth > y.depth;
+      return x.path > y.path;
+    };
+    std::unique_ptr<Alg4> a(new Alg4);
+    uint64_t dmsk[kDoneChecks];
+    int dval[kDoneChecks];
+    for (int m = 2; m <= 64; ++m) {
+      std::priority_queue<Node, std::vector<Node>, decltype(later)> heap(later);
+      heap.push(Node{0.0, 0, 0});
+      std::vector<Node> nodes;
+      while (!heap.empty() && (int)nodes.size() < kPlan) {
+        const Node x = heap.top();
+        heap.pop();
+        int dn = 0;
+        if (!alg4_replay(*a, m, x.path, x.depth, dmsk, dval, dn)) continue;  // the machine finishes first
+        if (x.depth > 0) nodes.push_back(x);
+        if (x.depth >= 63) continue;
+        const double p = a->req == kReqCover ? kPlanPassRelaxed : kPlanPassExact;
+        heap.push(Node{x.nl - std::log2(p), x.path | (1ull << x.depth), x.depth + 1});
+        heap.push(Node{x.nl - std::log2(1.0 - p), x.path, x.depth + 1});
+      }
+      int32_t* st = pl.data() + m * (kPlanLevels + 1);
+      int32_t* nd = pl.data() + kPlanNodeWord + m * kPlan * 4;
+      int l = 0;
+      for (int j = 0; j < (int)nodes.size(); ++j) {
+        const int lvl = std::min(kPlanLevels - 1, (int)(2.0 * nodes[j].nl));
+        while (l <= lvl) st[l++] = j;
+        nd[4 * j] = nodes[j].depth;
+        nd[4 * j + 1] = lvl;
+        nd[4 * j + 2] = (int32_t)(uint32_t)nodes[j].path;
+        nd[4 * j + 3] = (int32_t)(uint32_t)(nodes[j].path >> 32);
+      }
+      while (l <= kPlanLevels) st[l++] = (int)nodes.size();
+    }
+    return pl;
+  }();
+  return plan;
+}
+
 epic_status upload(epic_ctx* c) {
   const HostTables& H = c->H;
   std::vector<char> blob;
@@ -1112,7 +1206,7 @@ epic_status upload(epic_ctx* c) {
          o_lhs = place(blob, H.item_lhs), o_nsym = place(blob, H.next_sym), o_mn = place(blob, H.mn),
          o_gtm = place(blob, H.gap_tm), o_gown = place(blob, H.gap_own), o_ccl = place(blob, H.cover_cl),
          o_enib = place(blob, H.expn_nib), o_pnib = place(blob, H.pred_nib), o_gcov = place(blob, H.gap_cover),
-         o_lnib = place(blob, H.lhs_nib), o_snib = place(blob, H.sym_nib), o_psnib = place(blob, H.predsym_nib),
+         o_lnib = place(blob, H.lhs_nib), o_snib = place(blob, H.sym_nib), o_psnib = place(blob, H.predsym_nib), o_plan = place(blob, speculation_plan()),
          o_vb = place(blob, H.vbytes), o_vo = place(blob, H.voffs), o_endof = place(blob, H.end_of),
          o_dot0 = place(blob, H.dot0), o_wynt = place(blob, H.wy_nt), o_wyown = place(blob, H.wy_own),
          o_wypool = place(blob, H.wy_pool);
@@ -1179,6 +1273,7 @@ epic_status upload(epic_ctx* c) {
   t.lhs_nib = (const uint64_t*)(d + o_lnib);
   t.sym_nib = (const uint64_t*)(d + o_snib);
   t.predsym_nib = (const uint64_t*)(d + o_psnib);
+  t.plan = (const int32_t*)(d + o_plan);
   t.cover_cl = (const uint32_t*)(d + o_ccl);
   t.vbytes = (const uint8_t*)(d + o_vb);
   t.voffs = (const int32_t*)(d + o_vo);
@@ -1403,7 +1498,7 @@ epic_status SelectLaunch<W>::run(epic_ctx* c, const int32_t* seqs, int B, int n,
   }
   if (grid > B) {
     KernelTimer kt(c, kKSpecClear, stream);
-    hipLaunchKernelGGL(spec_account_kernel<W>, dim3((B * kSpec + 255) / 256), dim3(256), 0, stream, spec, B,
+    hipLaunchKernelGGL(spec_account_kernel<W>, dim3((B * kPlan + 255) / 256), dim3(256), 0, stream, spec, B,
                        tb.work, tab_for(c, kKSelectHelp).work);
   }
   return hipGetLastError() == hipSuccess ? EPIC_OK : EPIC_ERR_HIP;
