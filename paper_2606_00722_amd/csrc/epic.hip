@@ -759,8 +759,8 @@ EPIC_INLINE int select_walk(const DevTab& tb, Lds<W>& L, const WgWork& wk, const
 // (sequence, node) pairs level by level, sequence by sequence within a
 // level.  A helper replays the machine along its node's path to learn the
 // node's check (or that the machine finishes before it), walks it and
-// publishes the result with a state word (0 not started, 1 running, 2 done,
-// 3 no check there).  The selection looks up the node of its own path: it
+// publishes the result in a state word (0 not started, 1 running, 3 no check
+// there, 4 + the outcome when done).  The selection looks up the node of its own path: it
 // takes a result that is done, waits for one that is running (its helper
 // is resident and finishes on its own), and otherwise walks the check
 // itself.  The plan decides only which checks run early: a helper's result
@@ -778,9 +778,13 @@ constexpr int kPlanWords = kPlanNodeWord + 65 * kPlan * 4;
 // walk of the launch slower (C-like 256-token selection 29.8 -> 31.3 ms).
 constexpr int kSpecHelpers = 5;
 // Speculation block of a selection launch over B sequences (int32 words):
-// state [B*kPlan], result [B*kPlan], consulted flag [B*kPlan], then the work
-// counters of each speculated check's walk (uint64 [B*kPlan][6]).
-constexpr int spec_work_word(int B) { return (3 * B * kPlan + 1) & ~1; }
+// state [B*kPlan], consulted flag [B*kPlan], then the work counters of each
+// speculated check's walk (uint64 [B*kPlan][6]).  A state word carries the
+// result too (kSpecDone + outcome, or kSpecDone + 2 when the walk ran out of
+// capacity), so that publishing and reading it need no cache write-back or
+// invalidation: one relaxed agent-scope store, relaxed polls.
+enum : int { kSpecIdle = 0, kSpecRunning = 1, kSpecNone = 3, kSpecDone = 4 };
+constexpr int spec_work_word(int B) { return (2 * B * kPlan + 1) & ~1; }
 constexpr int spec_words(int B) { return spec_work_word(B) + 2 * 6 * B * kPlan; }
 constexpr long long kSpecWaitCycles = 4ll << 30;  // give up waiting on a helper after this many clocks
 constexpr int kSpecSeqs = 128;  // sequences a launch with helpers may hold
@@ -812,7 +816,7 @@ __global__ void spec_account_kernel(const int32_t* __restrict__ spec, int B, uns
   if (i >= B * kPlan) return;
   const unsigned long long* w = reinterpret_cast<const unsigned long long*>(spec + spec_work_word(B)) + (size_t)i * 6;
   if (w[0] == 0) return;
-  unsigned long long* to = spec[2 * B * kPlan + i] ? used : unused;
+  unsigned long long* to = spec[B * kPlan + i] ? used : unused;
   for (int k = 0; k < 6; ++k) atomicAdd(&to[k], w[k]);
 }
 
@@ -832,9 +836,8 @@ __global__ void __launch_bounds__(NT) select_kernel(DevTab tb, const int32_t* __
   __shared__ int done_n, done_hit, spec_pick, plan_j;
   const WgWork wk = slot_work(ws, blockIdx.x);
   stage_tables<W>(tb, L);
-  int32_t* spec_state = spec;                 // [B * kPlan]
-  int32_t* spec_res = spec + B * kPlan;       // [B * kPlan]
-  int32_t* spec_used = spec + 2 * B * kPlan;  // [B * kPlan]: the selection took the result
+  int32_t* spec_state = spec;             // [B * kPlan]
+  int32_t* spec_used = spec + B * kPlan;  // [B * kPlan]: the selection took the result
   // Workgroups b < B run Alg. 4 for sequence b; the others are helpers, each
   // walking the check of one planned node of a sequence b.  Both reach the
   // walks through the one call site of each check type below.
@@ -895,7 +898,7 @@ __global__ void __launch_bounds__(NT) select_kernel(DevTab tb, const int32_t* __
         found = alg4_replay(M, m, path, e[0], done_msk, done_val, done_n);
       }
       plan_j = found ? 1 : 0;
-      __hip_atomic_store(&spec_state[b * kPlan + hj], found ? 1 : 3, found ? __ATOMIC_RELAXED : __ATOMIC_RELEASE,
+      __hip_atomic_store(&spec_state[b * kPlan + hj], found ? kSpecRunning : kSpecNone, __ATOMIC_RELAXED,
                          __HIP_MEMORY_SCOPE_AGENT);
     }
     __syncthreads();
@@ -954,14 +957,9 @@ __global__ void __launch_bounds__(NT) select_kernel(DevTab tb, const int32_t* __
           int res = -1;
           const long long t_start = (long long)clock64();
           while ((long long)clock64() - t_start < kSpecWaitCycles) {
-            // relaxed polls, one acquire fence when the result is there (an
-            // acquire load per poll would invalidate this XCD's L2 each time)
             const int st = __hip_atomic_load(&spec_state[b * kPlan + q], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            if (st == 2) {
-              __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-              res = __hip_atomic_load(&spec_res[b * kPlan + q], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            }
-            if (st != 1) break;
+            if (st == kSpecDone || st == kSpecDone + 1) res = st - kSpecDone;
+            if (st != kSpecRunning) break;
             __builtin_amdgcn_s_sleep(8);
           }
           if (res >= 0) spec_used[b * kPlan + q] = 1;
@@ -979,8 +977,9 @@ __global__ void __launch_bounds__(NT) select_kernel(DevTab tb, const int32_t* __
                            : select_walk<W, false, SHARE>(tb, L, wk, ws, seqs, n, b, msk);
     if (helper) {
       if (threadIdx.x == 0) {
-        spec_res[b * kPlan + hj] = r < 0 ? -1 : r;  // capacity: the selection walks it again and reports
-        __hip_atomic_store(&spec_state[b * kPlan + hj], 2, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+        // capacity (r < 0): the selection walks the check again and reports it
+        __hip_atomic_store(&spec_state[b * kPlan + hj], kSpecDone + (r < 0 ? 2 : r), __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
       }
       return;
     }
