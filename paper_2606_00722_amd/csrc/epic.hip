@@ -751,27 +751,27 @@ EPIC_INLINE int select_walk(const DevTab& tb, Lds<W>& L, const WgWork& wk, const
 // form one binary decision tree per m.  A node is a path of outcomes: those
 // of the checks before it that were not found among the answered checks.
 // The root, the relaxed check of all candidates, is the selection's own
-// first walk.  For every m the host lists the nodes below the root by
+// first walk.  For every m the host explores the tree below the root by
 // decreasing estimated probability (outcomes taken as independent, a
-// relaxed check passing with probability 0.62, an exact one with 0.79), at
-// most kPlan of them, each with a level: twice the negative base-2
-// logarithm of that probability, rounded down.  Helper workgroups take
-// (sequence, node) pairs level by level, sequence by sequence within a
-// level.  A helper replays the machine along its node's path to learn the
-// node's check (or that the machine finishes before it), walks it and
-// publishes the result in a state word (0 not started, 1 running, 3 no check
-// there, 4 + the outcome when done).  The selection looks up the node of its own path: it
-// takes a result that is done, waits for one that is running (its helper
-// is resident and finishes on its own), and otherwise walks the check
-// itself.  The plan decides only which checks run early: a helper's result
-// is that of the check the machine asks at its node.
+// relaxed check passing with probability 0.62, an exact one with 0.79) and
+// lists the first kPlan distinct checks (kind and subset) it meets, each
+// with a level: twice the negative base-2 logarithm of that probability,
+// rounded down.  Helper workgroups take (sequence, planned check) pairs
+// level by level, sequence by sequence within a level, walk the check and
+// publish the result in a state word (0 not started, 1 running, 3 nothing to
+// do, 4 + the outcome when done).  When the selection needs a check, it
+// looks it up among the planned checks of its m: it takes a result that is
+// done, waits for one that is running (its helper is resident and finishes
+// on its own), and otherwise walks the check itself.  A check's outcome
+// depends only on its kind and subset, so the plan decides only which
+// checks run early, not any result.
 constexpr int kPlan = 64;        // planned nodes (state slots) per sequence
 constexpr int kPlanLevels = 32;  // levels of the helper order
 constexpr double kPlanPassRelaxed = 0.62, kPlanPassExact = 0.79;
-// Plan table (int32 words): level starts [65][kPlanLevels + 1] (the nodes of
-// m at level l are kPlan*m + start[l] .. start[l+1]-1; start[kPlanLevels] is
-// their count), then the nodes [65][kPlan] as {depth, level, path low word,
-// path high word}.
+// Plan table (int32 words): level starts [65][kPlanLevels + 1] (the checks
+// of m at level l are kPlan*m + start[l] .. start[l+1]-1; start[kPlanLevels]
+// is their count), then the checks [65][kPlan] as {kind (kReqCover or
+// kReqExact), level, subset low word, subset high word}.
 constexpr int kPlanNodeWord = 65 * (kPlanLevels + 1);
 constexpr int kPlanWords = kPlanNodeWord + 65 * kPlan * 4;
 // Helpers per sequence at most: more (up to 15 at 16 sequences) made every
@@ -889,13 +889,13 @@ __global__ void __launch_bounds__(NT) select_kernel(DevTab tb, const int32_t* __
   const int bad = select_setup<W>(tb, L, seqs, n, cseq, cpos, ctok, conf, verdict, C, b, helper ? nullptr : selected);
   if (helper) {
     if (threadIdx.x == 0) {
-      // the node's check: the machine replayed along the node's path
       const int m = L.sel_n;
       bool found = false;
       if (!bad && m >= 2 && m <= 64 && hj < tb.plan[m * (kPlanLevels + 1) + kPlanLevels]) {
         const int32_t* e = tb.plan + kPlanNodeWord + (m * kPlan + hj) * 4;
-        const uint64_t path = (uint64_t)(uint32_t)e[2] | ((uint64_t)(uint32_t)e[3] << 32);
-        found = alg4_replay(M, m, path, e[0], done_msk, done_val, done_n);
+        M.req = e[0];
+        M.mask = (uint64_t)(uint32_t)e[2] | ((uint64_t)(uint32_t)e[3] << 32);
+        found = true;
       }
       plan_j = found ? 1 : 0;
       __hip_atomic_store(&spec_state[b * kPlan + hj], found ? kSpecRunning : kSpecNone, __ATOMIC_RELAXED,
@@ -915,9 +915,6 @@ __global__ void __launch_bounds__(NT) select_kernel(DevTab tb, const int32_t* __
   if (!helper && L.sel_bad) return;
   long long ncover = 0, nexact = 0;
   bool failed = false;
-  // the path: outcomes of the checks so far that were not answered checks
-  int pdepth = 0;
-  uint64_t pbits = 0;
   for (int step = 0; step < 1 << 20; ++step) {
     int req;
     uint64_t msk;
@@ -942,14 +939,14 @@ __global__ void __launch_bounds__(NT) select_kernel(DevTab tb, const int32_t* __
       }
       __syncthreads();
       r = done_hit;
-      if (r < 0 && helpers && pdepth >= 1 && pdepth < 64) {
-        // the planned node of this path, if any
+      if (r < 0 && helpers && step > 0) {
+        // this check among the planned ones, if it is there
         const int m = L.sel_n;
         const int cnt = tb.plan[m * (kPlanLevels + 1) + kPlanLevels];
         for (int j = threadIdx.x; j < cnt; j += (int)blockDim.x) {
           const int32_t* e = tb.plan + kPlanNodeWord + (m * kPlan + j) * 4;
-          const uint64_t path = (uint64_t)(uint32_t)e[2] | ((uint64_t)(uint32_t)e[3] << 32);
-          if (e[0] == pdepth && path == pbits) plan_j = j;
+          const uint64_t sub = (uint64_t)(uint32_t)e[2] | ((uint64_t)(uint32_t)e[3] << 32);
+          if (e[0] == req && sub == msk) plan_j = j;
         }
         __syncthreads();
         const int q = plan_j;
@@ -971,7 +968,7 @@ __global__ void __launch_bounds__(NT) select_kernel(DevTab tb, const int32_t* __
         }
       }
     }
-    const bool fresh = done_hit < 0;  // not an answered check: the path grows
+    const bool fresh = done_hit < 0;
     if (r < 0)
       r = req == kReqCover ? select_walk<W, true, SHARE>(tb, L, wk, ws, seqs, n, b, msk)
                            : select_walk<W, false, SHARE>(tb, L, wk, ws, seqs, n, b, msk);
@@ -986,10 +983,6 @@ __global__ void __launch_bounds__(NT) select_kernel(DevTab tb, const int32_t* __
     if (r < 0) {
       failed = true;
       break;
-    }
-    if (fresh) {
-      if (pdepth < 64) pbits |= (uint64_t)r << pdepth;
-      ++pdepth;
     }
     if (threadIdx.x == 0) {
       M.res = r;
@@ -1142,10 +1135,11 @@ size_t place(std::vector<char>& blob, const std::vector<T>& v) {
   return off;
 }
 
-// The selection's speculation plan: for m = 2..64 candidates, the nodes of
-// the machine's decision tree below the root by decreasing estimated
-// probability, best first (a node's children are its check's two outcomes),
-// in the layout of kPlanWords.  The same for every context.
+// The selection's speculation plan: for m = 2..64 candidates, the distinct
+// checks met exploring the machine's decision tree below the root by
+// decreasing estimated probability, best first (a node's children are its
+// check's two outcomes), in the layout of kPlanWords.  The same for every
+// context.
 const std::vector<int32_t>& speculation_plan() {
   static const std::vector<int32_t> plan = [] {
     std::vector<int32_t> pl(kPlanWords, 0);
@@ -1166,12 +1160,17 @@ const std::vector<int32_t>& speculation_plan() {
       std::priority_queue<Node, std::vector<Node>, decltype(later)> heap(later);
       heap.push(Node{0.0, 0, 0});
       std::vector<Node> nodes;
-      while (!heap.empty() && (int)nodes.size() < kPlan) {
+      std::vector<std::pair<int, uint64_t>> checks;  // (kind, subset) of nodes[j]
+      for (int pops = 0; !heap.empty() && (int)nodes.size() < kPlan && pops < 1 << 16; ++pops) {
         const Node x = heap.top();
         heap.pop();
         int dn = 0;
         if (!alg4_replay(*a, m, x.path, x.depth, dmsk, dval, dn)) continue;  // the machine finishes first
-        if (x.depth > 0) nodes.push_back(x);
+        const std::pair<int, uint64_t> ck(a->req, a->mask);
+        if (x.depth > 0 && std::find(checks.begin(), checks.end(), ck) == checks.end()) {
+          nodes.push_back(x);
+          checks.push_back(ck);
+        }
         if (x.depth >= 63) continue;
         const double p = a->req == kReqCover ? kPlanPassRelaxed : kPlanPassExact;
         heap.push(Node{x.nl - std::log2(p), x.path | (1ull << x.depth), x.depth + 1});
@@ -1183,10 +1182,10 @@ const std::vector<int32_t>& speculation_plan() {
       for (int j = 0; j < (int)nodes.size(); ++j) {
         const int lvl = std::min(kPlanLevels - 1, (int)(2.0 * nodes[j].nl));
         while (l <= lvl) st[l++] = j;
-        nd[4 * j] = nodes[j].depth;
+        nd[4 * j] = checks[j].first;
         nd[4 * j + 1] = lvl;
-        nd[4 * j + 2] = (int32_t)(uint32_t)nodes[j].path;
-        nd[4 * j + 3] = (int32_t)(uint32_t)(nodes[j].path >> 32);
+        nd[4 * j + 2] = (int32_t)(uint32_t)checks[j].second;
+        nd[4 * j + 3] = (int32_t)(uint32_t)(checks[j].second >> 32);
       }
       while (l <= kPlanLevels) st[l++] = (int)nodes.size();
     }
