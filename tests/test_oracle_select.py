@@ -109,3 +109,46 @@ def test_selection_invariants(oracle_lib, preset, n):
                     assert set(chosen) == set(valid)
         W.commit(inst, pr, v, sel)
     assert nonempty >= 1
+
+
+@pytest.mark.parametrize("preset,n", [(1, 32), (2, 64), (3, 64), (5, 96)])
+def test_checks_are_monotone_in_the_filled_positions(oracle_lib, preset, n):
+    """A masked run reads any bytes (R1), so filling more masked positions
+    only shrinks the character language of x, and the regular cover's
+    language contains L(G).  Hence, for candidate sets T ⊆ S of one
+    sequence: x + S exact-valid => x + T exact-valid; x + S cover-valid =>
+    x + T cover-valid; x + S exact-valid => x + S cover-valid.  The device
+    selection answers a check that an answered check decides this way
+    without walking it; the oracle never does, so this pins the property on
+    the oracle's own checks."""
+    rng = np.random.default_rng(5)
+    inst = W.make_instance(preset, 23, B=6, n=n)
+    p = oracle_lib.problem_from(inst.lang, inst.vocab)
+    seen = {(k, r): 0 for k in ("e", "c") for r in (0, 1)}
+    for _ in range(2):
+        pr = W.propose(inst)
+        v = oracle_lib.validate_batch(p, inst.seqs, pr.seq, pr.pos, pr.tok)
+        for b in range(inst.B):
+            idx = np.flatnonzero((pr.seq == b) & (v == 1))
+            if idx.size < 2:
+                continue
+            for _ in range(6):
+                S = idx[rng.random(idx.size) < 0.7]
+                T = S[rng.random(S.size) < 0.5]
+                res = {}
+                for name, sub in (("S", S), ("T", T)):
+                    y = inst.seqs[b].copy()
+                    y[pr.pos[sub]] = pr.tok[sub]
+                    res[name] = (oracle_lib.valid(p, y), oracle_lib.cover(p, y))
+                for k, i in (("e", 0), ("c", 1)):
+                    seen[(k, res["S"][i])] += 1
+                    if res["S"][i] == 1:
+                        assert res["T"][i] == 1, (preset, b, S, T, k)
+                if res["S"][0] == 1:
+                    assert res["S"][1] == 1
+                if res["T"][1] == 0:
+                    assert res["T"][0] == 0
+        W.commit(inst, pr, v, oracle_lib.select(p, inst.seqs, pr.seq, pr.pos, pr.tok, pr.conf, v)[0])
+    assert sum(seen.values()) >= 20, seen
+    if preset == 2:  # the JSON-like workload's subsets fail both checks too
+        assert all(seen[(k, r)] for k in ("e", "c") for r in (0, 1)), seen
