@@ -556,6 +556,19 @@ __host__ __device__ inline int done_find(const uint64_t* msk, const int* val, in
   return hit;
 }
 
+// The outcome of a check (cover or exact, on subset m) that an answered
+// check (cover2, subset m2, outcome r2) decides, else -1.  A masked run
+// reads any bytes, so filling more positions only shrinks the character
+// language of x: checks are monotone in the subset (a pass carries to its
+// subsets, a failure to its supersets); and the cover's language contains
+// L(G), so an exact pass implies a cover pass and a cover failure an exact
+// failure.
+__host__ __device__ inline int implied_outcome(bool cover, uint64_t m, bool cover2, uint64_t m2, int r2) {
+  if (r2 == 1 && (m & ~m2) == 0 && (cover2 == cover || !cover2)) return 1;
+  if (r2 == 0 && (m2 & ~m) == 0 && (cover2 == cover || cover2)) return 0;
+  return -1;
+}
+
 // Replays the machine from its start along a path of outcomes (bit i: the
 // outcome of the i-th check not found in the answered checks) until the
 // check at depth d; false when the machine finishes first.  On true, a.req
@@ -833,7 +846,7 @@ __global__ void __launch_bounds__(NT) select_kernel(DevTab tb, const int32_t* __
   __shared__ Alg4 M;
   __shared__ uint64_t done_msk[kDoneChecks];
   __shared__ int done_val[kDoneChecks];  // result | (cover ? 2 : 0)
-  __shared__ int done_n, done_hit, spec_pick, plan_j;
+  __shared__ int done_n, done_hit, spec_pick, plan_j, implied;
   const WgWork wk = slot_work(ws, blockIdx.x);
   stage_tables<W>(tb, L);
   int32_t* spec_state = spec;             // [B * kPlan]
@@ -936,11 +949,39 @@ __global__ void __launch_bounds__(NT) select_kernel(DevTab tb, const int32_t* __
       if (threadIdx.x == 0) {
         done_hit = done_find(done_msk, done_val, done_n, msk, kind);
         plan_j = -1;
+        implied = -1;
       }
       __syncthreads();
       r = done_hit;
+      if (r < 0 && step > 0) {
+        // decided by an answered check: the selection's own, or a helper's
+        // finished one (all such answers agree)
+        const bool cov = req == kReqCover;
+        for (int k = threadIdx.x; k < done_n; k += (int)blockDim.x) {
+          const int o = implied_outcome(cov, msk, (done_val[k] & 2) != 0, done_msk[k], done_val[k] & 1);
+          if (o >= 0) implied = o;
+        }
+        if (helpers) {
+          const int m = L.sel_n;
+          const int cnt = tb.plan[m * (kPlanLevels + 1) + kPlanLevels];
+          for (int j = threadIdx.x; j < cnt; j += (int)blockDim.x) {
+            const int st = __hip_atomic_load(&spec_state[b * kPlan + j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (st != kSpecDone && st != kSpecDone + 1) continue;
+            const int32_t* e = tb.plan + kPlanNodeWord + (m * kPlan + j) * 4;
+            const uint64_t sub = (uint64_t)(uint32_t)e[2] | ((uint64_t)(uint32_t)e[3] << 32);
+            const int o = implied_outcome(cov, msk, e[0] == kReqCover, sub, st - kSpecDone);
+            if (o >= 0) {
+              implied = o;
+              spec_used[b * kPlan + j] = 1;
+            }
+          }
+        }
+        __syncthreads();
+        r = implied;
+      }
       if (r < 0 && helpers && step > 0) {
-        // this check among the planned ones, if it is there
+        // this check among the planned ones, if it is there (a running one:
+        // waited for; finished ones were looked at above)
         const int m = L.sel_n;
         const int cnt = tb.plan[m * (kPlanLevels + 1) + kPlanLevels];
         for (int j = threadIdx.x; j < cnt; j += (int)blockDim.x) {
