@@ -195,7 +195,10 @@ epic_status epic_validate_batch_noalloc(epic_ctx* ctx, const int32_t* d_seqs, in
  * EPIC_DEV_CAPACITY; a verdict-1 candidate that is not a legal update sets
  * EPIC_DEV_BAD_CANDIDATE.
  * d_counts (optional, device int64 [2]) accumulates the number of cover and
- * exact checks performed. */
+ * exact checks Alg. 4 calls.  Some calls are answered without a walk: a
+ * repeated check, or one an answered check decides (a pass carries to
+ * subsets, a failure to supersets, an exact pass to the cover check, a cover
+ * failure to the exact check); the answer is the one the walk would give. */
 epic_status epic_select_compatible(epic_ctx* ctx, const int32_t* d_seqs, int32_t B, int32_t n,
                                    const int32_t* d_cand_seq, const int32_t* d_cand_pos,
                                    const int32_t* d_cand_tok, const float* d_conf,
@@ -246,8 +249,8 @@ epic_status epic_ctx_set_timing(epic_ctx* ctx, int32_t enable);
 
 /* Diagnostics: synchronise `stream`, then read and clear, per kernel kind k
  * (0 lexing memo, 1 base walks of prefix sharing, 2 candidate walks of
- * validation, 3 selection (the checks Alg. 4 asks for, whether walked by the
- * selection's workgroup or taken from a helper's speculated walk),
+ * validation, 3 selection (the walks it used: its own, and the helpers'
+ * speculated walks whose results it took or drew an answer from),
  * 4 sequential fallback, 5 speculation bookkeeping (state clear, work
  * accounting), 6 speculated checks whose results the selection did not take
  * (no launches of their own, their time is the selection's)): ms[k]
