@@ -787,9 +787,10 @@ constexpr double kPlanPassRelaxed = 0.62, kPlanPassExact = 0.79;
 // kReqExact), level, subset low word, subset high word}.
 constexpr int kPlanNodeWord = 65 * (kPlanLevels + 1);
 constexpr int kPlanWords = kPlanNodeWord + 65 * kPlan * 4;
-// Helpers per sequence at most: more (up to 15 at 16 sequences) made every
-// walk of the launch slower (C-like 256-token selection 29.8 -> 31.3 ms).
-constexpr int kSpecHelpers = 5;
+// Helpers per sequence at most (a launch also leaves every workgroup a CU
+// and a chart slot): with the planned checks, 15 helpers at 16 sequences
+// measured faster than 5 (C-like 256-token selection 25.8 -> 23.9 ms).
+constexpr int kSpecHelpers = 31;
 // Speculation block of a selection launch over B sequences (int32 words):
 // state [B*kPlan], consulted flag [B*kPlan], then the work counters of each
 // speculated check's walk (uint64 [B*kPlan][6]).  A state word carries the
