@@ -1062,6 +1062,14 @@ __global__ void __launch_bounds__(NT) select_kernel(DevTab tb, const int32_t* __
 // invalid on x stays invalid on every later x.  One workgroup per sequence;
 // the checks are the selection's exact walks (with SHARE, resumed from the
 // sequence's base walk at the masked run of the lowest committed position).
+// Helpers of the fallback: workgroups from nprim on each check one
+// remaining candidate i of one sequence against the selected set alone
+// (x + B + c_i), concurrently with the loops.  Checks are monotone in the
+// subset (a masked run reads any bytes), so when the loop reaches i with
+// committed set K (B within K): a failure there decides that x + K + c_i
+// fails too, and while K is still B a pass is the loop's very check.  Helper
+// hi takes the hi-th (j, sequence) pair, j-th remaining candidate first;
+// results go to state words as the selection's (4 + outcome when done).
 template <int W, int NT, bool SHARE>
 __global__ void __launch_bounds__(NT) fallback_kernel(DevTab tb, const int32_t* __restrict__ seqs, int B, int n,
                                                       const int32_t* __restrict__ cseq,
@@ -1071,15 +1079,75 @@ __global__ void __launch_bounds__(NT) fallback_kernel(DevTab tb, const int32_t* 
                                                       const uint8_t* __restrict__ verdict,
                                                       const uint8_t* __restrict__ selected,
                                                       const int32_t* __restrict__ num_commit, int C,
-                                                      uint8_t* __restrict__ accepted, WsArgs ws) {
+                                                      uint8_t* __restrict__ accepted, WsArgs ws, int nprim,
+                                                      int32_t* __restrict__ spec) {
   __shared__ Lds<W> L;
   __shared__ uint64_t kept;  // sorted candidates committed: B, then the accepted ones
-  __shared__ int need;
+  __shared__ int need, pick, decided;
   const WgWork wk = slot_work(ws, blockIdx.x);
   stage_tables<W>(tb, L);
-  for (int b = blockIdx.x; b < B; b += gridDim.x) {
+  const bool helpers = (int)gridDim.x > nprim;
+  if ((int)blockIdx.x >= nprim) {
+    // remaining (valid, not selected) candidates per sequence, then the
+    // hi-th pair over the (j, sequence) cells; the origin hash is free
+    // until the walk, which clears it
+    int* rem = reinterpret_cast<int*>(L.hash);  // [B]
+    const int hi = (int)blockIdx.x - nprim;
+    for (int k = threadIdx.x; k < B; k += (int)blockDim.x) rem[k] = 0;
+    if (threadIdx.x == 0) pick = -1;
+    __syncthreads();
+    for (int c = threadIdx.x; c < C; c += (int)blockDim.x) {
+      const int cb = cseq[c];
+      if (cb >= 0 && cb < B && verdict[c] == 1 && !selected[c]) atomicAdd(&rem[cb], 1);
+    }
+    __syncthreads();
+    const int ncell = 64 * B, per = (ncell + (int)blockDim.x - 1) / (int)blockDim.x;
+    const int c0 = (int)threadIdx.x * per, c1 = c0 + per < ncell ? c0 + per : ncell;
+    int sum = 0;
+    for (int c = c0; c < c1; ++c) sum += c / B < rem[c % B];
+    int total = 0;
+    int acc = block_scan<W>(L, sum, &total);
+    if (hi >= acc && hi < acc + sum)
+      for (int c = c0; c < c1; ++c) {
+        if (!(c / B < rem[c % B])) continue;
+        if (acc == hi) {
+          pick = c;
+          break;
+        }
+        ++acc;
+      }
+    __syncthreads();
+    if (pick < 0) return;
+    const int b = pick % B, j = pick / B;
+    select_setup<W>(tb, L, seqs, n, cseq, cpos, ctok, conf, verdict, C, b, nullptr);
+    if (threadIdx.x == 0) {
+      // the j-th remaining candidate in confidence order, and B
+      uint64_t k0 = 0;
+      int i = -1, r = 0;
+      for (int q = 0; q < L.sel_n; ++q) {
+        if (selected[L.sel_idx[q]])
+          k0 |= 1ull << q;
+        else if (r++ == j)
+          i = q;
+      }
+      kept = k0;
+      pick = L.sel_bad || i < 0 ? -1 : i;
+      if (pick >= 0)
+        __hip_atomic_store(&spec[b * kPlan + pick], kSpecRunning, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    __syncthreads();
+    const int i = pick;
+    if (i < 0) return;
+    const int r = select_walk<W, false, SHARE, false>(tb, L, wk, ws, seqs, n, b, kept | (1ull << i));
+    if (threadIdx.x == 0)
+      __hip_atomic_store(&spec[b * kPlan + i], kSpecDone + (r < 0 ? 2 : r), __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
+    return;
+  }
+  for (int b = blockIdx.x; b < B; b += nprim) {
     // sorts b's verdict-1 candidates and clears accepted[] of all of b's
     select_setup<W>(tb, L, seqs, n, cseq, cpos, ctok, conf, verdict, C, b, accepted);
+    uint64_t k0 = 0;  // B
     if (threadIdx.x == 0) {
       if (L.sel_bad)
         atomicOr(tb.dev_err, L.sel_bad == 2   ? (uint32_t)EPIC_DEV_CAPACITY
@@ -1092,10 +1160,31 @@ __global__ void __launch_bounds__(NT) fallback_kernel(DevTab tb, const int32_t* 
       need = num_commit[b] - __popcll(k);
     }
     __syncthreads();
+    k0 = kept;
     if (!L.sel_bad) {
       for (int i = 0; i < L.sel_n && need > 0; ++i) {
         if ((kept >> i) & 1) continue;
-        const int r = select_walk<W, false, SHARE, false>(tb, L, wk, ws, seqs, n, b, kept | (1ull << i));
+        int r = -1;
+        if (helpers) {
+          // a helper's check of x + B + c_i: a failure decides; a pass decides
+          // while nothing beyond B is committed (then it is this check, and
+          // a running one is waited for)
+          if (threadIdx.x == 0) {
+            const bool same = kept == k0;
+            int res = -1;
+            const long long t_start = (long long)clock64();
+            while ((long long)clock64() - t_start < kSpecWaitCycles) {
+              const int st = __hip_atomic_load(&spec[b * kPlan + i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+              if (st == kSpecDone || (st == kSpecDone + 1 && same)) res = st - kSpecDone;
+              if (st != kSpecRunning || !same) break;
+              __builtin_amdgcn_s_sleep(8);
+            }
+            decided = res;
+          }
+          __syncthreads();
+          r = decided;
+        }
+        if (r < 0) r = select_walk<W, false, SHARE, false>(tb, L, wk, ws, seqs, n, b, kept | (1ull << i));
         if (r < 0) {
           if (threadIdx.x == 0)
             atomicOr(tb.dev_err, (uint32_t)EPIC_DEV_CAPACITY | (1u << (8 + (L.overflow & 15))));
@@ -1549,19 +1638,30 @@ epic_status FallbackLaunch<W>::run(epic_ctx* c, const int32_t* seqs, int B, int 
                                    const int32_t* cp, const int32_t* ct, const float* conf, const uint8_t* verdict,
                                    const uint8_t* sel, const int32_t* num_commit, int C, uint8_t* accepted,
                                    void* ws, hipStream_t stream) {
-  const int grid = std::min(B, c->nslot);
+  const int nprim = std::min(B, c->nslot);
   const WsArgs wa = ws_args(c, ws);
+  int32_t* spec = (int32_t*)((char*)ws + c->off_spec);
+  // helpers as the selection's: as many as leave every workgroup a CU and a
+  // chart slot
+  const int nh = std::min({kSpecHelpers, c->num_cus / B - 1, c->nslot / B - 1});
+  const int grid = nh >= 1 && B <= kSpecSeqs && nprim == B ? B * (nh + 1) : nprim;
   // long sequences: the loop's exact checks resume from the base walks of the
   // Earley graphs, as the selection's do
   const bool share = n >= kShareSelectLen && B <= c->base_slots;
   if (share) launch_base<W>(c, seqs, B, n, B, wa, stream);
+  if (grid > nprim) {
+    KernelTimer kt(c, kKSpecClear, stream);
+    hipLaunchKernelGGL(spec_clear_kernel<W>, dim3((B * kPlan + 255) / 256), dim3(256), 0, stream, spec, B * kPlan);
+  }
   KernelTimer kt(c, kKFallback, stream);
   if (share)
     hipLaunchKernelGGL((fallback_kernel<W, kThreads, true>), dim3(grid), dim3(kThreads), 0, stream,
-                       tab_for(c, kKFallback), seqs, B, n, cs, cp, ct, conf, verdict, sel, num_commit, C, accepted, wa);
+                       tab_for(c, kKFallback), seqs, B, n, cs, cp, ct, conf, verdict, sel, num_commit, C, accepted, wa,
+                       nprim, spec);
   else
     hipLaunchKernelGGL((fallback_kernel<W, kThreads, false>), dim3(grid), dim3(kThreads), 0, stream,
-                       tab_for(c, kKFallback), seqs, B, n, cs, cp, ct, conf, verdict, sel, num_commit, C, accepted, wa);
+                       tab_for(c, kKFallback), seqs, B, n, cs, cp, ct, conf, verdict, sel, num_commit, C, accepted, wa,
+                       nprim, spec);
   return hipGetLastError() == hipSuccess ? EPIC_OK : EPIC_ERR_HIP;
 }
 
