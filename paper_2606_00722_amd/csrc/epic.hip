@@ -94,12 +94,19 @@ __global__ void __launch_bounds__(kMemoThreads) lexmemo_kernel(DevTab tb, uint4*
   const size_t i = (size_t)blockIdx.x * kMemoThreads + threadIdx.x;
   if (i >= (size_t)tb.V * tb.Q) return;
   const int t = (int)(i / tb.Q), q0 = (int)(i % tb.Q);
-  const int beg = tb.voffs[t], len = tb.voffs[t + 1] - beg;
+  const int beg = tb.voffs[t], len = tb.voffs[t + 1] - beg;  // 1..8 bytes (checked at create)
+  // the token's bytes first, all loads in flight together; then the chain of
+  // transitions
+  int by[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) by[j] = j < len ? tb.vbytes[beg + j] : 0;
   int q = q0;
   uint32_t n = 0, mask = 0, lab_lo = 0, lab_hi = 0;
   bool dead = false;
-  for (int j = 0; j < len; ++j) {
-    const int c = tb.vbytes[beg + j];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    if (j >= len) break;
+    const int c = by[j];
     const int d = tb.trans[q * 256 + c];
     if (d >= 0) {
       q = d;
