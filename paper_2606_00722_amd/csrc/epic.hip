@@ -750,18 +750,23 @@ EPIC_INLINE int select_walk_body(const DevTab& tb, Lds<W>& L, const WgWork& wk, 
 // threads, on checks resumed from base walks, 4.12 against 4.44 ms per
 // 1024-token step.  Narrower item sets, and the sequential fallback, inline
 // it.
+// It takes the walk slot's index, not its descriptor: a descriptor passed by
+// reference would live in per-lane scratch, and the walk would read its
+// pointers from there.
 template <int W, bool COVER, bool SHARE>
-__device__ __attribute__((noinline)) int select_walk_call(const DevTab& tb, Lds<W>& L, const WgWork& wk,
-                                                          const WsArgs& ws, const int32_t* __restrict__ seqs, int n,
-                                                          int b, uint64_t msk) {
+__device__ __attribute__((noinline)) int select_walk_call(const DevTab& tb, Lds<W>& L, int slot, const WsArgs& ws,
+                                                          const int32_t* __restrict__ seqs, int n, int b,
+                                                          uint64_t msk) {
+  const WgWork wk = slot_work(ws, slot);
   return select_walk_body<W, COVER, SHARE>(tb, L, wk, ws, seqs, n, b, msk);
 }
 
+// `wk` is the workgroup's own walk slot (slot_work(ws, blockIdx.x)).
 template <int W, bool COVER, bool SHARE, bool CALL = (W >= 16)>
 EPIC_INLINE int select_walk(const DevTab& tb, Lds<W>& L, const WgWork& wk, const WsArgs& ws,
                                   const int32_t* __restrict__ seqs, int n, int b, uint64_t msk) {
   if constexpr (CALL)
-    return select_walk_call<W, COVER, SHARE>(tb, L, wk, ws, seqs, n, b, msk);
+    return select_walk_call<W, COVER, SHARE>(tb, L, (int)blockIdx.x, ws, seqs, n, b, msk);
   else
     return select_walk_body<W, COVER, SHARE>(tb, L, wk, ws, seqs, n, b, msk);
 }
