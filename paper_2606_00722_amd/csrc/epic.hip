@@ -1255,6 +1255,7 @@ struct epic_ctx {
   uint32_t epoch = 0;  // launches of base and candidate walks together (walk-record progress words)
   void* scratch = nullptr;  // this device's static scratch (epic_validate_batch_noalloc)
   // witness workspace layout, per sequence (epic_witness)
+  int wit_lds_proofs = kWitLdsSlots / 2;  // proofs indexed in LDS by the back-trace
   size_t wit_stride = 0, wit_rec = 0, wit_mark = 0, wit_stack = 0, wit_w = 0, wit_recs = 0, wit_vis = 0;
   size_t wit_proof = 0, wit_pindex = 0, wit_sys = 0;
   int wit_ecap = 0;
@@ -1485,6 +1486,7 @@ WitArgs wit_args(const epic_ctx* c, void* wws) {
   a.rcap = kWitRecords;
   a.vwords = kWitVisWords;
   a.steps = kWitSteps;
+  a.lproofs = c->wit_lds_proofs;
   return a;
 }
 
@@ -1834,6 +1836,13 @@ epic_status epic_ctx_work_counters(epic_ctx* c, hipStream_t stream, int64_t* out
 epic_status epic_ctx_set_timing(epic_ctx* c, int32_t enable) {
   if (!c) return EPIC_ERR_NULL;
   c->timing = enable != 0;
+  return EPIC_OK;
+}
+
+epic_status epic_ctx_set_witness_lds_proofs(epic_ctx* c, int32_t max_proofs) {
+  if (!c) return EPIC_ERR_NULL;
+  if (max_proofs < 0 || max_proofs > kWitLdsSlots / 2) return EPIC_ERR_ARG;
+  c->wit_lds_proofs = max_proofs;
   return EPIC_OK;
 }
 
