@@ -247,14 +247,17 @@ epic_status epic_ctx_work_counters(epic_ctx* ctx, hipStream_t stream, int64_t* o
  * Off by default. */
 epic_status epic_ctx_set_timing(epic_ctx* ctx, int32_t enable);
 
-/* Witness extraction (failure recovery, Sec. 4): how many proofs the
- * back-trace indexes in LDS before it moves its proof index to the witness
- * workspace for the rest of that sequence's search (0 = the workspace's index
- * from the start).  Where the index lives does not change the search or its
- * result, only its speed.  0 <= max_proofs <= 8192 (the default), else
- * EPIC_ERR_ARG and the setting is unchanged.  Applies to later
- * epic_witness calls on the context. */
-epic_status epic_ctx_set_witness_lds_proofs(epic_ctx* ctx, int32_t max_proofs);
+/* Witness extraction (failure recovery, Sec. 4): how much of the search
+ * state lives in LDS rather than in the witness workspace.  The back-trace
+ * indexes up to max_proofs proofs in LDS, then moves its proof index to the
+ * workspace for the rest of that sequence's search (0: the workspace's index
+ * from the start); the byte search keeps a masked run's visited set in LDS
+ * when it fits in max_vis_words 32-bit words, else in the workspace.  Where
+ * they live changes only the speed, not which completions can be found.
+ * 0 <= max_proofs <= 8192 and 0 <= max_vis_words <= 4096 (the defaults are
+ * the maxima), else EPIC_ERR_ARG and the settings are unchanged.  Applies to
+ * later epic_witness calls on the context. */
+epic_status epic_ctx_set_witness_lds(epic_ctx* ctx, int32_t max_proofs, int32_t max_vis_words);
 
 /* Diagnostics: synchronise `stream`, then read and clear, per kernel kind k
  * (0 lexing memo, 1 base walks of prefix sharing, 2 candidate walks of

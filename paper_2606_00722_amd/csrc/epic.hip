@@ -1256,6 +1256,7 @@ struct epic_ctx {
   void* scratch = nullptr;  // this device's static scratch (epic_validate_batch_noalloc)
   // witness workspace layout, per sequence (epic_witness)
   int wit_lds_proofs = kWitLdsSlots / 2;  // proofs indexed in LDS by the back-trace
+  int wit_lds_vis = kWitVisLds;           // visited-set words of a masked run kept in LDS
   size_t wit_stride = 0, wit_rec = 0, wit_mark = 0, wit_stack = 0, wit_w = 0, wit_recs = 0, wit_vis = 0;
   size_t wit_proof = 0, wit_pindex = 0, wit_sys = 0;
   int wit_ecap = 0;
@@ -1487,6 +1488,7 @@ WitArgs wit_args(const epic_ctx* c, void* wws) {
   a.vwords = kWitVisWords;
   a.steps = kWitSteps;
   a.lproofs = c->wit_lds_proofs;
+  a.lvis = c->wit_lds_vis;
   return a;
 }
 
@@ -1839,10 +1841,12 @@ epic_status epic_ctx_set_timing(epic_ctx* c, int32_t enable) {
   return EPIC_OK;
 }
 
-epic_status epic_ctx_set_witness_lds_proofs(epic_ctx* c, int32_t max_proofs) {
+epic_status epic_ctx_set_witness_lds(epic_ctx* c, int32_t max_proofs, int32_t max_vis_words) {
   if (!c) return EPIC_ERR_NULL;
-  if (max_proofs < 0 || max_proofs > kWitLdsSlots / 2) return EPIC_ERR_ARG;
+  if (max_proofs < 0 || max_proofs > kWitLdsSlots / 2 || max_vis_words < 0 || max_vis_words > kWitVisLds)
+    return EPIC_ERR_ARG;
   c->wit_lds_proofs = max_proofs;
+  c->wit_lds_vis = max_vis_words;
   return EPIC_OK;
 }
 

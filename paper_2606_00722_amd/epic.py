@@ -27,7 +27,7 @@ FUNCTIONS = ["epic_ctx_create", "epic_ctx_destroy", "epic_workspace_bytes", "epi
              "epic_select_compatible",
              "epic_commit_fallback",
              "epic_ctx_device_error", "epic_ctx_work_counters", "epic_ctx_set_timing",
-             "epic_ctx_set_witness_lds_proofs", "epic_ctx_kernel_stats",
+             "epic_ctx_set_witness_lds", "epic_ctx_kernel_stats",
              "epic_witness_workspace_bytes", "epic_witness",
              "epic_diag_lds_stream", "epic_diag_clock_rates", "epic_status_string"]
 KERNEL_KINDS = ["lexmemo", "base", "validate", "select", "fallback", "spec_bookkeeping", "spec_unused"]
@@ -91,8 +91,8 @@ def lib() -> ctypes.CDLL:
         L.epic_ctx_work_counters.restype = ctypes.c_int
         L.epic_ctx_set_timing.argtypes = [P, i32]
         L.epic_ctx_set_timing.restype = ctypes.c_int
-        L.epic_ctx_set_witness_lds_proofs.argtypes = [P, i32]
-        L.epic_ctx_set_witness_lds_proofs.restype = ctypes.c_int
+        L.epic_ctx_set_witness_lds.argtypes = [P, i32, i32]
+        L.epic_ctx_set_witness_lds.restype = ctypes.c_int
         L.epic_ctx_kernel_stats.argtypes = [P, P, P, P, P]
         L.epic_ctx_kernel_stats.restype = ctypes.c_int
         L.epic_witness_workspace_bytes.argtypes = [P, i32]
@@ -253,8 +253,8 @@ class Context:
     def set_timing(self, enable: bool = True):
         _check("epic_ctx_set_timing", lib().epic_ctx_set_timing(self._h, int(bool(enable))))
 
-    def set_witness_lds_proofs(self, max_proofs: int):
-        _check("epic_ctx_set_witness_lds_proofs", lib().epic_ctx_set_witness_lds_proofs(self._h, int(max_proofs)))
+    def set_witness_lds(self, max_proofs: int = 8192, max_vis_words: int = 4096):
+        _check("epic_ctx_set_witness_lds", lib().epic_ctx_set_witness_lds(self._h, int(max_proofs), int(max_vis_words)))
 
     def kernel_stats(self, stream=None) -> dict:
         """Per kernel kind (KERNEL_KINDS): summed event ms, launches and the

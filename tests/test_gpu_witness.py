@@ -27,13 +27,13 @@ def gpu_mod():
     return gpu_util
 
 
-def run_witness(gpu_mod, lang, vocab, seqs, max_cands=64, lds_proofs=None):
+def run_witness(gpu_mod, lang, vocab, seqs, max_cands=64, lds=None):
     import torch
 
     B, n = seqs.shape
     g = gpu_mod.Gpu(W.arrays(lang, vocab), B, n, max(max_cands, B))
-    if lds_proofs is not None:
-        g.ctx.set_witness_lds_proofs(lds_proofs)
+    if lds is not None:
+        g.ctx.set_witness_lds(*lds)
     wws = g.ctx.alloc_witness_workspace(B, g.dev)
     cap, max_gaps = 1 << 14, n
     out = torch.zeros((B, cap), dtype=torch.uint8, device=g.dev)
@@ -87,34 +87,35 @@ def test_witness_workload_sequences(preset, gpu_mod, oracle_lib):
     assert all(s == 1 for s in sts[:inst.B])
 
 
-def test_witness_proof_index_placement(gpu_mod, oracle_lib):
-    """Where the back-trace keeps its proof index (LDS throughout, moved to the
-    workspace after 300 proofs, or the workspace from the start) does not
-    change the outcome: the statuses are equal and every completion parses.
-    (The bytes themselves can differ from call to call: the byte search's
-    breadth-first records are appended by many threads at once.)"""
+def test_witness_search_state_placement(gpu_mod, oracle_lib):
+    """Where the witness search keeps its state (the back-trace's proof index:
+    LDS throughout, moved to the workspace after 300 proofs, or the workspace
+    from the start; the byte search's visited sets: LDS or the workspace) does
+    not change the outcome: the statuses are equal and every completion
+    parses.  (The bytes themselves can differ from call to call: the byte
+    search's breadth-first records are appended by many threads at once.)"""
     inst = W.make_instance(3, 42, B=6)
     p = oracle_lib.problem_from(inst.lang, inst.vocab)
     seqs = inst.seqs.astype(np.int32)
-    for k in (None, 300, 0):
-        res, err = run_witness(gpu_mod, inst.lang, inst.vocab, seqs, lds_proofs=k)
+    for lds in (None, (300, 4096), (0, 0), (8192, 0)):
+        res, err = run_witness(gpu_mod, inst.lang, inst.vocab, seqs, lds=lds)
         assert err == 0
         for b in range(seqs.shape[0]):
             st, gaps = res[b]
             check(oracle_lib, p, inst.lang, inst.vocab.strings, seqs[b], st, gaps, independent=False)
-            assert st == 1, (k, b)
+            assert st == 1, (lds, b)
 
 
-def test_witness_lds_proofs_range(gpu_mod):
+def test_witness_lds_range(gpu_mod):
     from paper_2606_00722_amd import epic
 
     inst = W.make_instance(1, 42, B=2)
     g = gpu_mod.Gpu(W.arrays(inst.lang, inst.vocab), 2, inst.n, 64)
-    for bad in (-1, 8193):
+    for bad in ((-1, 0), (8193, 0), (0, -1), (0, 4097)):
         with pytest.raises(epic.EpicError):
-            g.ctx.set_witness_lds_proofs(bad)
-    g.ctx.set_witness_lds_proofs(8192)
-    g.ctx.set_witness_lds_proofs(0)
+            g.ctx.set_witness_lds(*bad)
+    g.ctx.set_witness_lds(8192, 4096)
+    g.ctx.set_witness_lds(0, 0)
 
 
 @pytest.mark.parametrize("name", ["tiny_paren", "tiny_expr", "tiny_kw", "tiny_ab", "arith"])
